@@ -1,0 +1,167 @@
+"""Seeded synthetic workloads for one host's share of APB prefill attention.
+
+This module is shared by the GPU path, the oracle-based tests and the bench.
+It draws random numbers and rounds them to the storage formats; it holds none
+of the method's arithmetic (no attention, no selection, no masking).
+
+Shapes follow the paper's problem statement: a host holds an anchor block of
+La rows (query tokens plus the first l_a document tokens, Sec. 3.3), a local
+block of Lb = l_b rows (Sec. 3.3), and receives l_p compressed rows from each
+previous host (Sec. 3.4-3.5).  ``host_idx`` is 0-based and equals the number
+of previous hosts, so the passing block holds Lp = host_idx * l_p rows.
+
+Every tensor is head-major ``[heads, rows, d]`` with d contiguous, stored as
+bf16 bit patterns (``uint16``).  Scores are fp32 ``[n_kv, Lb]``.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+
+@dataclasses.dataclass(frozen=True)
+class Problem:
+    """One host's share of one attention layer (Alg. 2 inputs)."""
+
+    n_hosts: int
+    host_idx: int
+    anchor_len: int
+    local_len: int
+    pass_len: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+
+    @property
+    def rows(self) -> int:
+        """Query rows on this host: anchor then local block (Eq. 2)."""
+        return self.anchor_len + self.local_len
+
+    @property
+    def passing_rows(self) -> int:
+        """Lp: compressed rows received from the host_idx previous hosts."""
+        return self.host_idx * self.pass_len
+
+    @property
+    def key_rows(self) -> int:
+        return self.anchor_len + self.passing_rows + self.local_len
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """A named problem plus the value distributions used to fill it."""
+
+    name: str
+    problem: Problem
+    outlier_k: bool = False  # 2% of K channels scaled x8
+    zipf_scores: bool = False  # scores ~ Zipf(1.5) instead of N(0, 1)
+
+
+# The five workloads: a tiny case, and layers shaped like Llama-3.1-8B,
+# Qwen-2.5-14B and Yi-34B at the context lengths and l_a / l_p / l_b the
+# paper uses (App. B, Table of sequence hyperparameters; Sec. 4.1 model list).
+WORKLOADS = {
+    "tiny": Workload(
+        "tiny", Problem(4, 2, 128, 512, 32, 4, 1, 64)),
+    "llama8b_32k": Workload(
+        "llama8b_32k", Problem(4, 3, 2048, 8192, 1024, 32, 8, 128)),
+    "llama8b_128k": Workload(
+        "llama8b_128k", Problem(8, 7, 4096, 16384, 2048, 32, 8, 128),
+        outlier_k=True),
+    "qwen14b_256k": Workload(
+        "qwen14b_256k", Problem(8, 7, 4096, 32768, 4096, 40, 8, 128)),
+    "yi34b_512k": Workload(
+        "yi34b_512k", Problem(8, 7, 8192, 65536, 8192, 56, 8, 128),
+        zipf_scores=True),
+}
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 to bf16 (round to nearest, ties to even); return uint16 bits."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))
+    return (rounded >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to fp32 (used only for display
+    and by generators that post-scale values; never by the oracle)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _normal_bf16(rng: np.random.Generator, shape, scale_cols=None) -> np.ndarray:
+    """N(0,1) fp32 draws rounded to bf16, drawn head by head so that a
+    prefix of heads never depends on how many heads follow."""
+    out = np.empty(shape, dtype=np.uint16)
+    for h in range(shape[0]):
+        x = rng.standard_normal(shape[1:], dtype=np.float32)
+        if scale_cols is not None:
+            x[..., scale_cols[h]] *= np.float32(8.0)
+        out[h] = f32_to_bf16_bits(x)
+    return out
+
+
+def outlier_channels(prob: Problem, seed: int) -> np.ndarray:
+    """ceil(2% of d) K channels per KV head, chosen by a seeded RNG."""
+    n_out = math.ceil(0.02 * prob.head_dim)
+    rng = np.random.default_rng(np.random.SeedSequence(seed).spawn(7)[6])
+    return np.stack([np.sort(rng.choice(prob.head_dim, n_out, replace=False))
+                     for _ in range(prob.n_kv_heads)])
+
+
+def make_inputs(wl: Workload, seed: int = 0) -> dict:
+    """Generate every input of one host share.
+
+    Per-tensor streams come from ``SeedSequence(seed).spawn(7)`` in the order
+    Q, K, V, K_pass, V_pass, scores, outlier channels.  Returns a dict with
+    ``q`` [n_q, La+Lb, d], ``k``/``v`` [n_kv, La+Lb, d] (local rows start at
+    La), ``k_pass``/``v_pass`` [host_idx, n_kv, l_p, d] (rank-major slots of
+    the earlier hosts' compressed blocks), all bf16 bits, and ``scores``
+    fp32 [n_kv, Lb].
+    """
+    p = wl.problem
+    ss = np.random.SeedSequence(seed).spawn(7)
+    cols = outlier_channels(p, seed) if wl.outlier_k else None
+    q = _normal_bf16(np.random.default_rng(ss[0]), (p.n_q_heads, p.rows, p.head_dim))
+    k = _normal_bf16(np.random.default_rng(ss[1]), (p.n_kv_heads, p.rows, p.head_dim), cols)
+    v = _normal_bf16(np.random.default_rng(ss[2]), (p.n_kv_heads, p.rows, p.head_dim))
+    kp_rng = np.random.default_rng(ss[3])
+    vp_rng = np.random.default_rng(ss[4])
+    k_pass = np.empty((p.host_idx, p.n_kv_heads, p.pass_len, p.head_dim), np.uint16)
+    v_pass = np.empty_like(k_pass)
+    for s in range(p.host_idx):
+        k_pass[s] = _normal_bf16(kp_rng, k_pass.shape[1:], cols)
+        v_pass[s] = _normal_bf16(vp_rng, v_pass.shape[1:])
+    s_rng = np.random.default_rng(ss[5])
+    if wl.zipf_scores:
+        scores = s_rng.zipf(1.5, size=(p.n_kv_heads, p.local_len)).astype(np.float32)
+    else:
+        scores = s_rng.standard_normal((p.n_kv_heads, p.local_len), dtype=np.float32)
+    return dict(q=q, k=k, v=v, k_pass=k_pass, v_pass=v_pass, scores=scores,
+                outlier_cols=cols)
+
+
+def make_host_blocks(wl: Workload, seed: int = 0) -> list:
+    """Synthetic local blocks of every earlier host (for the multi-host
+    simulation): for host j < host_idx, K/V [n_kv, La+Lb, d] and scores
+    [n_kv, Lb].  Stream ``SeedSequence(seed + 1000 + j)``."""
+    p = wl.problem
+    cols = outlier_channels(p, seed) if wl.outlier_k else None
+    out = []
+    for j in range(p.host_idx):
+        ss = np.random.SeedSequence(seed + 1000 + j).spawn(3)
+        k = _normal_bf16(np.random.default_rng(ss[0]), (p.n_kv_heads, p.rows, p.head_dim), cols)
+        v = _normal_bf16(np.random.default_rng(ss[1]), (p.n_kv_heads, p.rows, p.head_dim))
+        rng = np.random.default_rng(ss[2])
+        if wl.zipf_scores:
+            sc = rng.zipf(1.5, size=(p.n_kv_heads, p.local_len)).astype(np.float32)
+        else:
+            sc = rng.standard_normal((p.n_kv_heads, p.local_len), dtype=np.float32)
+        out.append(dict(k=k, v=v, scores=sc))
+    return out
