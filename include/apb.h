@@ -1,0 +1,144 @@
+/*
+ * apb.h -- C ABI of one host's share of APB prefill attention on MI355X.
+ *
+ * APB (Accelerating distributed long-context inference by Passing compressed
+ * context Blocks) splits a long document across H hosts.  Host h holds an
+ * anchor block A (query tokens plus the first document tokens, Sec. 3.3), its
+ * local block B_h (Sec. 3.3), and receives from every earlier host a
+ * compressed block of l_p key/value rows chosen by a compressor (Sec. 3.4),
+ * which together form the passing block P (Sec. 3.5).  Attention then runs
+ * over queries [A; B_h] and keys/values [A; P; B_h] under a modified mask
+ * (Sec. 3.6, Eq. 2).
+ *
+ * This library exports the two kernels of that host share:
+ *   apb_compress_select  ArgTop-l_p of the local block's scores + gather of
+ *                        the selected K/V rows (Sec. 3.4; Alg. 2, compression
+ *                        step);
+ *   apb_attention_fwd    the modified-mask attention (Eq. 2; Alg. 2,
+ *                        attention step).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are caller-owned DEVICE memory on the current HIP
+ *     device.  The library never allocates, frees or keeps them.
+ *   - bf16 tensors are passed as uint16_t bit patterns.  Layouts are
+ *     head-major, row-major, head_dim contiguous, densely packed.  bf16
+ *     tensors must be 16-byte aligned; fp32 and int32 tensors 4-byte aligned.
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
+ *     is the default stream), stateless and re-entrant.  No host sync.
+ *   - Every argument is validated on the host BEFORE any HIP call; a call
+ *     that returns an error has launched nothing and written nothing.
+ *   - Index arithmetic is 64-bit; a problem must satisfy
+ *     La + host_idx*l_p + Lb <= 2^30 rows.
+ *   - Outputs must not overlap inputs (checked: APB_ERR_ALIAS).
+ */
+#ifndef APB_H_
+#define APB_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define APB_ABI_VERSION 1
+
+typedef enum {
+  APB_OK = 0,
+  APB_ERR_NULL_POINTER = 1, /* a required pointer is NULL                    */
+  APB_ERR_BAD_SHAPE = 2,    /* a size violates the constraints below         */
+  APB_ERR_UNSUPPORTED = 3,  /* valid in the paper, not built here (head_dim) */
+  APB_ERR_MISALIGNED = 4,   /* a pointer breaks the alignment rule           */
+  APB_ERR_HIP = 5,          /* the HIP runtime reported a launch error       */
+  APB_ERR_ALIAS = 6         /* an output overlaps an input                   */
+} apb_status_t;
+
+/* One host's share of one attention layer: the inputs of Alg. 2 (l_p, h, H)
+ * and of Alg. 1 (l_a, l_p, h, H), plus the attention head geometry. */
+typedef struct {
+  int32_t n_hosts;    /* H >= 1: hosts the document is split over (Sec. 3.3) */
+  int32_t host_idx;   /* 0 <= host_idx < H, 0-based; equals the number of
+                         previous hosts (the paper's h is host_idx + 1)      */
+  int32_t anchor_len; /* La = l_q + l_a >= 0 anchor rows (Sec. 3.3); 0 for
+                         the first host or the no-anchor ablation           */
+  int32_t local_len;  /* Lb = l_b >= 1 rows of the local block (Sec. 3.3)   */
+  int32_t pass_len;   /* 0 <= l_p <= Lb rows each host passes on (Sec. 3.4) */
+  int32_t n_q_heads;  /* n_q >= 1, a multiple of n_kv                       */
+  int32_t n_kv_heads; /* n_kv >= 1; query head i reads KV head i / (n_q/n_kv) */
+  int32_t head_dim;   /* d, in {64, 128}                                     */
+} apb_problem_t;
+
+/*
+ * apb_compress_select -- the compressor C of Sec. 3.4 given the retaining
+ * heads' scores: ArgTop-l_p per KV head, then K^C = K_h[idx], V^C = V_h[idx]
+ * (Alg. 2, compression step).
+ *
+ *   scores  fp32 [n_kv][Lb]       importance of each local KV pair.
+ *   k, v    bf16 [n_kv][La+Lb][d] this host's keys/values; the local block
+ *                                 starts at row La.
+ *   out_idx int32 [n_kv][l_p]     selected local indices (0..Lb-1), ascending;
+ *                                 may be NULL.
+ *   out_k, out_v bf16 [n_kv][l_p][d]  bit copies of rows La+idx; typically
+ *                                 slot host_idx of a rank-major passing
+ *                                 buffer [H][n_kv][l_p][d].
+ * Selection: the l_p largest scores; equal scores (-0 equal to +0) go to the
+ * lower index; NaN ranks below -inf.  The result is unique, so it is
+ * bit-exact and deterministic.  l_p == 0 launches nothing and returns APB_OK.
+ */
+apb_status_t apb_compress_select(const apb_problem_t* p, const float* scores,
+                                 const uint16_t* k, const uint16_t* v,
+                                 int32_t* out_idx, uint16_t* out_k,
+                                 uint16_t* out_v, void* stream);
+
+/*
+ * apb_attention_fwd -- the modified-mask attention of Eq. 2 (Sec. 3.6):
+ * queries [A; B_h], keys/values [A; P; B_h] with P the earlier hosts'
+ * compressed blocks in host order (Sec. 3.5).  Mask M': causal attention over
+ * the concatenation [A; P; B_h] with the query rows of P removed, i.e. query
+ * row r sees concatenated keys 0..pos(r) where pos(r) = r for anchor rows
+ * (r < La) and r + host_idx*l_p for local rows.
+ *
+ *   q       bf16 [n_q][La+Lb][d]
+ *   k, v    bf16 [n_kv][La+Lb][d]            anchor rows then local rows.
+ *   k_pass, v_pass bf16 [host_idx][n_kv][l_p][d]  rank-major slots 0..host_idx-1
+ *                                 of the all-gathered compressed blocks
+ *                                 (Alg. 2, communication step); required
+ *                                 when host_idx*l_p > 0, ignored otherwise.
+ *   o       bf16 [n_q][La+Lb][d]  softmax-weighted values, rounded to nearest
+ *                                 even.
+ *   lse     fp32 [n_q][La+Lb]     natural log of the sum of exp(scaled
+ *                                 logits) per row, the quantity an LSE merge
+ *                                 of partial results needs (Alg. 3); may be
+ *                                 NULL.
+ *   softmax_scale  multiplier of Q.K; <= 0, NaN or inf selects 1/sqrt(d)
+ *                  (Eq. 1, d_m = head_dim).
+ * Arithmetic: bf16 inputs, fp32 dot products and softmax, probabilities
+ * rounded to bf16 for the value product, fp32 accumulation.
+ */
+apb_status_t apb_attention_fwd(const apb_problem_t* p, const uint16_t* q,
+                               const uint16_t* k, const uint16_t* v,
+                               const uint16_t* k_pass, const uint16_t* v_pass,
+                               uint16_t* o, float* lse, float softmax_scale,
+                               void* stream);
+
+/* Host-only checks of a problem description (no HIP call). */
+apb_status_t apb_validate_problem(const apb_problem_t* p);
+
+/* Unmasked attention FLOPs of one call: 4*d per visible (query, key) pair
+ * per query head, visible pairs La(La+1)/2 + Lb(La+Lp) + Lb(Lb+1)/2 with
+ * Lp = host_idx*l_p.  Host-only; returns -1 for an invalid problem. */
+double apb_attention_flops(const apb_problem_t* p);
+
+/* Static text for a status code (never NULL). */
+const char* apb_status_string(int status);
+
+/* Text of the last HIP error seen by this thread ("" if none). */
+const char* apb_last_error(void);
+
+/* APB_ABI_VERSION of the built library. */
+int apb_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* APB_H_ */

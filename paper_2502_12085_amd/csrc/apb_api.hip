@@ -1,0 +1,167 @@
+// C-ABI layer of the APB host-share library: argument validation (host only,
+// before any HIP call), status strings, the FLOP count, and dispatch to the
+// gfx950 kernels.
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/apb.h"
+#include "apb_internal.h"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+void set_last_error(hipError_t e) {
+  const char* msg = hipGetErrorString(e);
+  size_t i = 0;
+  for (; msg && msg[i] && i + 1 < sizeof(g_last_error); ++i) g_last_error[i] = msg[i];
+  g_last_error[i] = '\0';
+}
+
+constexpr int64_t kMaxRows = int64_t(1) << 30;
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range_of(const void* ptr, int64_t bytes) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
+  return Range{lo, lo + static_cast<uintptr_t>(bytes)};
+}
+
+bool overlaps(Range a, Range b) {
+  if (a.lo == a.hi || b.lo == b.hi || a.lo == 0 || b.lo == 0) return false;
+  return a.lo < b.hi && b.lo < a.hi;
+}
+
+bool aligned(const void* ptr, uintptr_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int apb_abi_version(void) { return APB_ABI_VERSION; }
+
+const char* apb_last_error(void) { return g_last_error; }
+
+const char* apb_status_string(int status) {
+  switch (status) {
+    case APB_OK: return "ok";
+    case APB_ERR_NULL_POINTER: return "a required pointer is NULL";
+    case APB_ERR_BAD_SHAPE: return "a size violates the problem constraints";
+    case APB_ERR_UNSUPPORTED: return "unsupported configuration (head_dim must be 64 or 128)";
+    case APB_ERR_MISALIGNED: return "a pointer is not aligned (bf16: 16 bytes, fp32/int32: 4 bytes)";
+    case APB_ERR_HIP: return "the HIP runtime reported an error";
+    case APB_ERR_ALIAS: return "an output overlaps an input";
+    default: return "unknown status";
+  }
+}
+
+apb_status_t apb_validate_problem(const apb_problem_t* p) {
+  if (!p) return APB_ERR_NULL_POINTER;
+  if (p->n_hosts < 1 || p->host_idx < 0 || p->host_idx >= p->n_hosts) return APB_ERR_BAD_SHAPE;
+  if (p->anchor_len < 0 || p->local_len < 1) return APB_ERR_BAD_SHAPE;
+  if (p->pass_len < 0 || p->pass_len > p->local_len) return APB_ERR_BAD_SHAPE;
+  if (p->n_kv_heads < 1 || p->n_q_heads < 1 || p->n_q_heads % p->n_kv_heads != 0)
+    return APB_ERR_BAD_SHAPE;
+  if (p->head_dim < 1) return APB_ERR_BAD_SHAPE;
+  const int64_t rows = (int64_t)p->anchor_len + (int64_t)p->host_idx * p->pass_len +
+                       (int64_t)p->local_len;
+  if (rows > kMaxRows) return APB_ERR_BAD_SHAPE;
+  // Grid size: query tiles of 128 rows times query heads must fit a 1-D grid.
+  const int64_t tiles = ((int64_t)p->anchor_len + p->local_len + 127) / 128 * p->n_q_heads;
+  if (tiles >= (int64_t(1) << 31)) return APB_ERR_BAD_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 128) return APB_ERR_UNSUPPORTED;
+  return APB_OK;
+}
+
+double apb_attention_flops(const apb_problem_t* p) {
+  if (apb_validate_problem(p) != APB_OK) return -1.0;
+  const double la = p->anchor_len, lb = p->local_len;
+  const double lp = (double)p->host_idx * p->pass_len;
+  const double pairs = la * (la + 1) / 2 + lb * (la + lp) + lb * (lb + 1) / 2;
+  return 4.0 * p->head_dim * p->n_q_heads * pairs;
+}
+
+apb_status_t apb_compress_select(const apb_problem_t* p, const float* scores, const uint16_t* k,
+                                 const uint16_t* v, int32_t* out_idx, uint16_t* out_k,
+                                 uint16_t* out_v, void* stream) {
+  const apb_status_t st = apb_validate_problem(p);
+  if (st != APB_OK) return st;
+  if (!scores || !k || !v || !out_k || !out_v) return APB_ERR_NULL_POINTER;
+  if (!aligned(scores, 4) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out_k, 16) ||
+      !aligned(out_v, 16) || (out_idx && !aligned(out_idx, 4)))
+    return APB_ERR_MISALIGNED;
+  const int64_t d = p->head_dim, nkv = p->n_kv_heads, lp = p->pass_len;
+  const int64_t kv_bytes = nkv * ((int64_t)p->anchor_len + p->local_len) * d * 2;
+  const Range in[3] = {range_of(scores, nkv * p->local_len * 4), range_of(k, kv_bytes),
+                       range_of(v, kv_bytes)};
+  const Range out[3] = {range_of(out_idx, out_idx ? nkv * lp * 4 : 0),
+                        range_of(out_k, nkv * lp * d * 2), range_of(out_v, nkv * lp * d * 2)};
+  for (const Range& o : out) {
+    for (const Range& i : in)
+      if (overlaps(o, i)) return APB_ERR_ALIAS;
+  }
+  if (overlaps(out[0], out[1]) || overlaps(out[0], out[2]) || overlaps(out[1], out[2]))
+    return APB_ERR_ALIAS;
+  if (lp == 0) return APB_OK;
+
+  apb::CompressArgs a;
+  a.scores = scores; a.k = k; a.v = v; a.idx = out_idx; a.out_k = out_k; a.out_v = out_v;
+  a.La = p->anchor_len; a.Lb = p->local_len; a.lp = p->pass_len;
+  a.n_kv = p->n_kv_heads; a.head_dim = p->head_dim;
+  const hipError_t e = apb::launch_compress(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    set_last_error(e);
+    return APB_ERR_HIP;
+  }
+  return APB_OK;
+}
+
+apb_status_t apb_attention_fwd(const apb_problem_t* p, const uint16_t* q, const uint16_t* k,
+                               const uint16_t* v, const uint16_t* k_pass,
+                               const uint16_t* v_pass, uint16_t* o, float* lse,
+                               float softmax_scale, void* stream) {
+  const apb_status_t st = apb_validate_problem(p);
+  if (st != APB_OK) return st;
+  const int64_t Lp = (int64_t)p->host_idx * p->pass_len;
+  if (!q || !k || !v || !o) return APB_ERR_NULL_POINTER;
+  if (Lp > 0 && (!k_pass || !v_pass)) return APB_ERR_NULL_POINTER;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
+      (lse && !aligned(lse, 4)))
+    return APB_ERR_MISALIGNED;
+  if (Lp > 0 && (!aligned(k_pass, 16) || !aligned(v_pass, 16))) return APB_ERR_MISALIGNED;
+  const int64_t d = p->head_dim, M = (int64_t)p->anchor_len + p->local_len;
+  const int64_t q_bytes = (int64_t)p->n_q_heads * M * d * 2;
+  const int64_t kv_bytes = (int64_t)p->n_kv_heads * M * d * 2;
+  const int64_t pass_bytes = Lp > 0 ? Lp * p->n_kv_heads * d * 2 : 0;
+  const Range in[5] = {range_of(q, q_bytes), range_of(k, kv_bytes), range_of(v, kv_bytes),
+                       range_of(Lp > 0 ? k_pass : nullptr, pass_bytes),
+                       range_of(Lp > 0 ? v_pass : nullptr, pass_bytes)};
+  const Range out[2] = {range_of(o, q_bytes),
+                        range_of(lse, lse ? (int64_t)p->n_q_heads * M * 4 : 0)};
+  for (const Range& r : out)
+    for (const Range& i : in)
+      if (overlaps(r, i)) return APB_ERR_ALIAS;
+  if (overlaps(out[0], out[1])) return APB_ERR_ALIAS;
+
+  float scale = softmax_scale;
+  if (!(scale > 0.f) || !isfinite(scale)) scale = 1.f / sqrtf((float)p->head_dim);
+  apb::AttnArgs a;
+  a.q = q; a.k = k; a.v = v;
+  a.kp = Lp > 0 ? k_pass : nullptr;
+  a.vp = Lp > 0 ? v_pass : nullptr;
+  a.o = o; a.lse = lse;
+  a.La = p->anchor_len; a.Lb = p->local_len; a.lp = p->pass_len; a.Lp = (int32_t)Lp;
+  a.n_q = p->n_q_heads; a.n_kv = p->n_kv_heads; a.head_dim = p->head_dim;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const hipError_t e = apb::launch_attention(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    set_last_error(e);
+    return APB_ERR_HIP;
+  }
+  return APB_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,186 @@
+// Compressor of one APB host (Sec. 3.4; Alg. 2, compression step) for gfx950:
+// ArgTop-l_p of the retaining-head scores of every KV head, then the gather
+// K^C = K_h[idx], V^C = V_h[idx].
+//
+// Design.  A grid of (S, n_kv) workgroups; workgroup (c, h) owns the local
+// index range chunk c of KV head h.  Every workgroup of a head first finds
+// the same selection threshold by an MSB-first radix select over all Lb
+// scores (four 8-bit digits of an order-preserving 32-bit key; the scores of
+// one head are a few hundred KB at most and stay in L2), so no scratch memory,
+// atomics across workgroups or second launch are needed.  It then counts
+// what was selected before its chunk and compacts its chunk in index order
+// (wave ballot + mbcnt prefix counts, a 4-wave LDS scan), which yields the
+// ascending output order and the lower-index-wins tie rule directly.  The
+// selected rows are copied with 16-byte vector loads and stores.
+#include "apb_internal.h"
+
+namespace apb {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+// Order-preserving map of an fp32 score to an unsigned key: a larger score
+// gives a larger key, -0 maps with +0, NaN maps to 0 (below -inf, whose key
+// is 0x007fffff).
+__device__ __forceinline__ uint32_t score_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Exclusive prefix count of `pred` over the 256 threads of the block, in
+// thread order; also returns the block total.  Uses `scan` (kWaves words).
+__device__ __forceinline__ uint32_t block_exclusive_count(bool pred, uint32_t* scan,
+                                                          uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long bal = __ballot(pred);
+  const uint32_t in_wave = __builtin_amdgcn_mbcnt_hi(
+      (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+  if (lane == 0) scan[wave] = (uint32_t)__popcll(bal);
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t c = scan[w];
+    before += (w < wave) ? c : 0u;
+    all += c;
+  }
+  __syncthreads();
+  *total = all;
+  return before + in_wave;
+}
+
+__global__ void __launch_bounds__(kThreads)
+topk_gather_kernel(const float* __restrict__ scores, const uint16_t* __restrict__ k,
+                   const uint16_t* __restrict__ v, int32_t* __restrict__ out_idx,
+                   uint16_t* __restrict__ out_k, uint16_t* __restrict__ out_v,
+                   int La, int Lb, int lp, int head_dim, int chunk) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t scan[kWaves];
+  __shared__ uint32_t sel_digit, sel_above;
+  __shared__ int32_t list_src[kThreads];
+  __shared__ int32_t list_dst[kThreads];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int head = blockIdx.y;
+  const float* s = scores + (size_t)head * Lb;
+
+  // ---- 1. radix select: key T of the lp-th largest score, and how many of
+  //         the scores equal to T are selected (`need`, >= 1).
+  uint32_t prefix = 0u, prefix_mask = 0u, remaining = (uint32_t)lp;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    hist[tid] = 0u;
+    __syncthreads();
+    for (int i = tid; i < Lb; i += kThreads) {
+      const uint32_t key = score_key(s[i]);
+      if ((key & prefix_mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid < 64) {
+      // lane L owns bins 4L..4L+3; suffix sums over lanes find the bin
+      // holding the remaining-th largest key.
+      uint32_t c[4], own = 0u;
+      for (int j = 0; j < 4; ++j) { c[j] = hist[4 * lane + j]; own += c[j]; }
+      uint32_t incl = own;  // inclusive suffix sum over lanes >= lane
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = __shfl_down(incl, off);
+        if (lane + off < 64) incl += o;
+      }
+      const uint32_t above_lane = incl - own;
+      if (above_lane < remaining && remaining <= incl) {
+        uint32_t above = above_lane;
+        for (int j = 3; j >= 0; --j) {
+          if (remaining <= above + c[j]) {
+            sel_digit = (uint32_t)(4 * lane + j);
+            sel_above = above;
+            break;
+          }
+          above += c[j];
+        }
+      }
+    }
+    __syncthreads();
+    prefix |= sel_digit << shift;
+    prefix_mask |= 255u << shift;
+    remaining -= sel_above;
+    __syncthreads();
+  }
+  const uint32_t T = prefix;
+  const uint32_t need = remaining;
+
+  // ---- 2. selected elements before this workgroup's chunk.
+  const int c0 = blockIdx.x * chunk;
+  const int c1 = min(Lb, c0 + chunk);
+  if (c0 >= c1) return;
+  uint32_t gt_before = 0u, eq_before = 0u;
+  for (int base = 0; base < c0; base += kThreads) {
+    const int i = base + tid;
+    const uint32_t key = (i < c0) ? score_key(s[i]) : 0u;
+    uint32_t tg, te;
+    block_exclusive_count(i < c0 && key > T, scan, &tg);
+    block_exclusive_count(i < c0 && key == T, scan, &te);
+    gt_before += tg;
+    eq_before += te;
+  }
+
+  // ---- 3. compaction of the chunk in index order + row gather.
+  const int row_chunks = head_dim / 8;  // 16-byte pieces per row
+  const size_t M = (size_t)La + Lb;
+  const uint4* ksrc = reinterpret_cast<const uint4*>(k + (size_t)head * M * head_dim);
+  const uint4* vsrc = reinterpret_cast<const uint4*>(v + (size_t)head * M * head_dim);
+  uint4* kdst = reinterpret_cast<uint4*>(out_k + (size_t)head * lp * head_dim);
+  uint4* vdst = reinterpret_cast<uint4*>(out_v + (size_t)head * lp * head_dim);
+  for (int base = c0; base < c1; base += kThreads) {
+    const int i = base + tid;
+    const uint32_t key = (i < c1) ? score_key(s[i]) : 0u;
+    const bool gt = i < c1 && key > T;
+    const bool eq = i < c1 && key == T;
+    uint32_t tg, te;
+    const uint32_t gx = gt_before + block_exclusive_count(gt, scan, &tg);
+    const uint32_t ex = eq_before + block_exclusive_count(eq, scan, &te);
+    const uint32_t pos = gx + min(ex, need);
+    // pos < lp holds by construction (exactly lp elements are selected); the
+    // test keeps every store in bounds regardless.
+    const bool sel = (gt || (eq && ex < need)) && pos < (uint32_t)lp;
+    uint32_t nsel;
+    const uint32_t slot = block_exclusive_count(sel, scan, &nsel);
+    if (sel) {
+      if (out_idx) out_idx[(size_t)head * lp + pos] = i;
+      list_src[slot] = i;
+      list_dst[slot] = (int32_t)pos;
+    }
+    __syncthreads();
+    const int pieces = (int)nsel * row_chunks;
+    for (int e = tid; e < 2 * pieces; e += kThreads) {
+      const int which = e >= pieces;  // 0: K, 1: V
+      const int ee = e - which * pieces;
+      const int r = ee / row_chunks, ch = ee - r * row_chunks;
+      const size_t src = ((size_t)La + list_src[r]) * row_chunks + ch;
+      const size_t dst = (size_t)list_dst[r] * row_chunks + ch;
+      if (which) vdst[dst] = vsrc[src];
+      else kdst[dst] = ksrc[src];
+    }
+    gt_before += tg;
+    eq_before += te;
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_compress(const CompressArgs& a, hipStream_t stream) {
+  if (a.lp == 0) return hipSuccess;
+  // Enough workgroups per head to spread the gather over the chip, each
+  // owning at least 1024 local indices.
+  int splits = a.Lb / 1024;
+  splits = splits < 1 ? 1 : (splits > 32 ? 32 : splits);
+  const int chunk = (a.Lb + splits - 1) / splits;
+  dim3 grid(splits, a.n_kv);
+  hipLaunchKernelGGL(topk_gather_kernel, grid, dim3(kThreads), 0, stream, a.scores, a.k, a.v,
+                     a.idx, a.out_k, a.out_v, a.La, a.Lb, a.lp, a.head_dim, chunk);
+  return hipGetLastError();
+}
+
+}  // namespace apb

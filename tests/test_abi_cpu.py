@@ -1,0 +1,128 @@
+"""The C-ABI library loads and exports every symbol ``include/apb.h``
+declares, and every validation error is raised on the host before any HIP
+call (fake device addresses are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2502_12085_amd import apb, inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "apb.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(apb_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = apb.lib()
+    declared = _declared_functions()
+    assert set(declared) == set(apb.EXPORTED)
+    for name in declared:
+        assert hasattr(L, name), name
+    assert apb.abi_version() == 1
+
+
+def _prob(**kw):
+    base = dict(n_hosts=4, host_idx=2, anchor_len=128, local_len=512, pass_len=32,
+                n_q_heads=4, n_kv_heads=1, head_dim=64)
+    base.update(kw)
+    return apb.Problem(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), 0),
+    (dict(n_hosts=0, host_idx=0), 2),
+    (dict(host_idx=4), 2),
+    (dict(host_idx=-1), 2),
+    (dict(anchor_len=-1), 2),
+    (dict(local_len=0), 2),
+    (dict(pass_len=513), 2),
+    (dict(pass_len=-1), 2),
+    (dict(n_q_heads=6, n_kv_heads=4), 2),
+    (dict(n_kv_heads=0), 2),
+    (dict(head_dim=96), 3),
+    (dict(head_dim=256), 3),
+    (dict(anchor_len=0, host_idx=0), 0),
+    (dict(pass_len=0), 0),
+    (dict(anchor_len=1 << 29, local_len=1 << 29, pass_len=1, host_idx=3), 2),
+])
+def test_validate_problem(kw, code):
+    assert apb.lib().apb_validate_problem(ctypes.byref(_prob(**kw))) == code
+
+
+def test_flops_match_oracle_closed_form():
+    for wl in inputs.WORKLOADS.values():
+        p = wl.problem
+        ref = oracle.attention_flops(p.n_q_heads, p.head_dim, p.anchor_len, p.local_len,
+                                     p.passing_rows)
+        assert apb.attention_flops(p) == pytest.approx(ref, rel=1e-12)
+    assert apb.lib().apb_attention_flops(ctypes.byref(_prob(head_dim=96))) == -1.0
+    # the 128K Llama-8B-shaped host share: 7.284e12 unmasked FLOPs
+    assert apb.attention_flops(inputs.WORKLOADS["llama8b_128k"].problem) == pytest.approx(7.284e12, rel=1e-3)
+
+
+def test_status_strings():
+    L = apb.lib()
+    for s in range(7):
+        assert L.apb_status_string(s)
+    assert L.apb_status_string(99) == b"unknown status"
+
+
+# Fake, well-separated device addresses: validation must reject every call
+# below before touching them.
+A = 0x7F0000000000
+Q, K, V, KP, VP, O, LSE, SC, IDX, OK_, OV = (A + i * (1 << 36) for i in range(11))
+
+
+def _attn(p, q=Q, k=K, v=V, kp=KP, vp=VP, o=O, lse=LSE):
+    return apb.lib().apb_attention_fwd(ctypes.byref(p), q, k, v, kp, vp, o, lse, 0.0, None)
+
+
+def _comp(p, sc=SC, k=K, v=V, idx=IDX, ok=OK_, ov=OV):
+    return apb.lib().apb_compress_select(ctypes.byref(p), sc, k, v, idx, ok, ov, None)
+
+
+def test_attention_error_paths():
+    p = _prob()
+    assert apb.lib().apb_attention_fwd(None, Q, K, V, KP, VP, O, LSE, 0.0, None) == 1
+    assert _attn(p, q=None) == 1
+    assert _attn(p, o=None) == 1
+    assert _attn(p, kp=None) == 1           # passing block required when Lp > 0
+    assert _attn(p, q=Q + 8) == 4           # bf16 needs 16-byte alignment
+    assert _attn(p, kp=KP + 2) == 4
+    assert _attn(p, lse=LSE + 2) == 4
+    assert _attn(p, o=Q) == 6               # output aliases an input
+    assert _attn(p, o=K + 64) == 6
+    assert _attn(p, lse=V + 16) == 6
+    assert _attn(p, lse=O + 16) == 6        # outputs overlap each other
+    assert _attn(_prob(head_dim=96)) == 3
+    assert _attn(_prob(pass_len=600)) == 2
+
+
+def test_compress_error_paths():
+    p = _prob()
+    assert apb.lib().apb_compress_select(None, SC, K, V, IDX, OK_, OV, None) == 1
+    assert _comp(p, sc=None) == 1
+    assert _comp(p, ok=None) == 1
+    assert _comp(p, sc=SC + 2) == 4
+    assert _comp(p, ok=OK_ + 8) == 4
+    assert _comp(p, idx=IDX + 1) == 4
+    assert _comp(p, ok=K) == 6
+    assert _comp(p, idx=SC) == 6
+    assert _comp(p, ov=OK_ + 32) == 6
+    assert _comp(_prob(n_q_heads=3, n_kv_heads=2)) == 2
+    # l_p = 0 is valid and launches nothing
+    assert _comp(_prob(pass_len=0)) == 0
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    x = torch.zeros(4, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        apb.attention_fwd(inputs.WORKLOADS["tiny"].problem, x, x, x, x, x, x)
