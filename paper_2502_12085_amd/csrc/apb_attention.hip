@@ -26,7 +26,12 @@
 //  * Tile classes per wave: key tiles wholly visible to all 32 rows run with
 //    no mask, tiles crossing the diagonal are masked element-wise, tiles
 //    beyond every row's visible prefix are skipped.
-//  * Grid order puts the query tiles with the longest key prefix first.
+//  * Running max updated lazily (only when it grows by more than 2^8), so
+//    the O rescale is off the common path.
+//  * Grid order puts the query tiles with the longest key prefix first, and
+//    keeps a GQA group's workgroups on one XCD (one L2) when n_kv % 8 == 0.
+//  * __launch_bounds__(256, 2): at most 256 VGPRs, two waves per SIMD, so one
+//    wave's softmax overlaps the other wave's MFMAs.
 #include <math.h>
 
 #include "apb_internal.h"
@@ -51,8 +56,30 @@ struct Params {
   float* lse;
   int La, Lb, lp, Lp, M, Ktot;
   int n_q, n_kv, group, n_qtiles;
+  int xcd_map;  // 1: every XCD serves whole KV-head groups (n_kv % 8 == 0)
   float scale_log2;
 };
+
+constexpr int kXcds = 8;           // MI355X: 8 XCDs, workgroups dealt round-robin
+constexpr float kRescaleSlack = 8.f;  // lazy rescale threshold, base-2 units
+
+// Workgroup -> (query head, query tile).  Tiles with the longest key prefix
+// go first.  With xcd_map, consecutive workgroup ids land on different XCDs,
+// so the id is split into (xcd, slot) and XCD x serves KV heads x, x+8, ...:
+// the query heads of one GQA group at neighbouring tiles share one L2.
+__device__ __forceinline__ void map_block(const Params& p, int bid, int& head, int& qtile) {
+  if (p.xcd_map) {
+    const int xcd = bid % kXcds, slot = bid / kXcds;
+    const int per_tile = p.group * (p.n_kv / kXcds);
+    qtile = p.n_qtiles - 1 - slot / per_tile;
+    const int rem = slot - (slot / per_tile) * per_tile;
+    const int kv_local = rem / p.group;
+    head = (xcd + kXcds * kv_local) * p.group + (rem - kv_local * p.group);
+  } else {
+    head = bid % p.n_q;
+    qtile = p.n_qtiles - 1 - bid / p.n_q;
+  }
+}
 
 __device__ __forceinline__ int vis_end(int r, int La, int Lp) {
   return (r < La ? r : r + Lp) + 1;
@@ -80,7 +107,7 @@ __device__ __forceinline__ int vt_pos(int kk) {
 }
 
 template <int D>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kThreads, 2)
 attn_fwd_kernel(Params p) {
   constexpr int KST = D + 8;            // K tile row stride (bf16 elements)
   constexpr int VST = kBN + 8;          // V^T tile row stride
@@ -99,9 +126,8 @@ attn_fwd_kernel(Params p) {
   const int lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
 
-  const int bid = blockIdx.x;
-  const int head = bid % p.n_q;
-  const int qtile = p.n_qtiles - 1 - bid / p.n_q;
+  int head, qtile;
+  map_block(p, blockIdx.x, head, qtile);
   const int kvh = head / p.group;
   const int r0 = qtile * kBM;
   const int r_last = min(r0 + kBM, p.M) - 1;
@@ -137,8 +163,50 @@ attn_fwd_kernel(Params p) {
   uint4 kbuf[K_LOADS];
   uint4 vbuf[V_LOADS][4];
 
+  // Global -> register staging of key tile t.  A tile that lies inside one
+  // segment (anchor, one passing slot, or local block) and below Ktot takes a
+  // single base address; tiles straddling a boundary fall back to per-row
+  // segment lookup.
   auto load_tile = [&](int t) {
     const int c0 = t * kBN;
+    const uint16_t* kbase = nullptr;
+    const uint16_t* vbase = nullptr;
+    if (c0 + kBN <= p.Ktot) {
+      if (c0 + kBN <= p.La) {
+        const size_t off = ((size_t)kvh * p.M + c0) * D;
+        kbase = p.k + off; vbase = p.v + off;
+      } else if (c0 >= p.La + p.Lp) {
+        const size_t off = ((size_t)kvh * p.M + (c0 - p.Lp)) * D;
+        kbase = p.k + off; vbase = p.v + off;
+      } else if (c0 >= p.La && c0 + kBN <= p.La + p.Lp) {
+        const int tt = c0 - p.La;
+        const int sl = tt / p.lp;
+        const int r = tt - sl * p.lp;
+        if (r + kBN <= p.lp) {
+          const size_t off = (((size_t)sl * p.n_kv + kvh) * p.lp + r) * D;
+          kbase = p.kp + off; vbase = p.vp + off;
+        }
+      }
+    }
+    if (kbase != nullptr) {
+      #pragma unroll
+      for (int i = 0; i < K_LOADS; ++i) {
+        const int e = tid + i * kThreads;
+        const int row = e / KCH, ch = e - row * KCH;
+        kbuf[i] = *reinterpret_cast<const uint4*>(kbase + (size_t)row * D + 8 * ch);
+      }
+      #pragma unroll
+      for (int i = 0; i < V_LOADS; ++i) {
+        const int e = tid + i * kThreads;
+        if (e < V_GROUPS) {
+          const int g = e / KCH, ch = e - g * KCH;
+          #pragma unroll
+          for (int j = 0; j < 4; ++j)
+            vbuf[i][j] = *reinterpret_cast<const uint4*>(vbase + (size_t)(4 * g + j) * D + 8 * ch);
+        }
+      }
+      return;
+    }
     #pragma unroll
     for (int i = 0; i < K_LOADS; ++i) {
       const int e = tid + i * kThreads;
@@ -237,24 +305,32 @@ attn_fwd_kernel(Params p) {
         #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[sb][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx * p.scale_log2);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
+      const float m_tile = mx * p.scale_log2;
+      // Lazy rescale: the running max m_run only moves when some row's tile
+      // max exceeds it by more than 2^kRescaleSlack, so exp2 arguments stay
+      // <= kRescaleSlack and O and l share the same (possibly stale) m_run;
+      // O / l and m_run*ln2 + ln(l) are unchanged by the choice of m_run.
+      if (__any(m_tile > m_run + kRescaleSlack)) {
+        const float m_new = fmaxf(m_run, m_tile);
+        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+        #pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          #pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      }
       float rs = 0.f;
       bf16x8 pb[4];
       #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
         #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_new));
+          const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
           rs += e;
           pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
         }
-      l_run = fmaf(l_run, alpha, rs);
-      #pragma unroll
-      for (int db = 0; db < NDB; ++db)
-        #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      l_run += rs;
       #pragma unroll
       for (int c = 0; c < 4; ++c)
         #pragma unroll
@@ -295,6 +371,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
   p.Ktot = a.La + a.Lp + a.Lb;
   p.n_q = a.n_q; p.n_kv = a.n_kv; p.group = a.n_q / a.n_kv;
   p.n_qtiles = (p.M + kBM - 1) / kBM;
+  p.xcd_map = (p.n_kv % kXcds) == 0;
   p.scale_log2 = a.scale_log2;
   const dim3 grid((unsigned)(p.n_qtiles * p.n_q));
   if (a.head_dim == 128)
