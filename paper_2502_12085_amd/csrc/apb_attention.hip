@@ -99,6 +99,15 @@ __device__ __forceinline__ const uint16_t* key_row(const Params& p, const uint16
   return loc + ((size_t)kvh * p.M + (c - p.Lp)) * D;
 }
 
+// Value held by the lane 32 apart (the other half of the wave holds the
+// other 16 keys of the same query in the 32x32 accumulator layout).
+__device__ __forceinline__ float half_swap(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  const int lane = threadIdx.x & 63;
+  return __uint_as_float(lane < 32 ? r[1] : r[0]);
+}
+
 // Position of key kk (0..63) of a tile inside a transposed V row: the keys a
 // lane-half contracts in one 16-key MFMA step become 8 contiguous entries.
 __device__ __forceinline__ int vt_pos(int kk) {
@@ -113,7 +122,10 @@ attn_fwd_kernel(Params p) {
   constexpr int VST = kBN + 8;          // V^T tile row stride
   constexpr int KCH = D / 8;            // 16-byte pieces per key row
   constexpr int K_LOADS = kBN * KCH / kThreads;          // per thread
-  constexpr int V_GROUPS = (kBN / 4) * KCH;              // (4 keys x 8 dims) groups
+  // V is staged in (4 keys x 8 dims) groups; consecutive lanes take
+  // consecutive key groups of one 8-dim chunk, so the transposed 8-byte LDS
+  // stores of 16 lanes hit 16 different bank pairs.
+  constexpr int V_GROUPS = (kBN / 4) * KCH;
   constexpr int V_LOADS = (V_GROUPS + kThreads - 1) / kThreads;
   constexpr int NKC = D / 16;           // MFMA k-steps over head_dim
   constexpr int NDB = D / 32;           // 32-wide blocks of head_dim in O^T
@@ -199,7 +211,7 @@ attn_fwd_kernel(Params p) {
       for (int i = 0; i < V_LOADS; ++i) {
         const int e = tid + i * kThreads;
         if (e < V_GROUPS) {
-          const int g = e / KCH, ch = e - g * KCH;
+          const int g = e % (kBN / 4), ch = e / (kBN / 4);
           #pragma unroll
           for (int j = 0; j < 4; ++j)
             vbuf[i][j] = *reinterpret_cast<const uint4*>(vbase + (size_t)(4 * g + j) * D + 8 * ch);
@@ -220,7 +232,7 @@ attn_fwd_kernel(Params p) {
     for (int i = 0; i < V_LOADS; ++i) {
       const int e = tid + i * kThreads;
       if (e < V_GROUPS) {
-        const int g = e / KCH, ch = e - g * KCH;
+        const int g = e % (kBN / 4), ch = e / (kBN / 4);
         #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int c = c0 + 4 * g + j;
@@ -243,7 +255,7 @@ attn_fwd_kernel(Params p) {
     for (int i = 0; i < V_LOADS; ++i) {
       const int e = tid + i * kThreads;
       if (e < V_GROUPS) {
-        const int g = e / KCH, ch = e - g * KCH;
+        const int g = e % (kBN / 4), ch = e / (kBN / 4);
         const int pos = vt_pos(4 * g);
         const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vbuf[i][0]);
         const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vbuf[i][1]);
@@ -304,7 +316,7 @@ attn_fwd_kernel(Params p) {
       for (int sb = 0; sb < 2; ++sb)
         #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[sb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = fmaxf(mx, half_swap(mx));
       const float m_tile = mx * p.scale_log2;
       // Lazy rescale: the running max m_run only moves when some row's tile
       // max exceeds it by more than 2^kRescaleSlack, so exp2 arguments stay
@@ -345,7 +357,7 @@ attn_fwd_kernel(Params p) {
   }
 
   if (!w_valid || rq >= p.M) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = l_run + half_swap(l_run);
   const float inv = 1.f / l_tot;
   uint16_t* orow = p.o + ((size_t)head * p.M + rq) * D;
   #pragma unroll
