@@ -9,29 +9,34 @@
 // concatenation is never materialised: key rows are fetched segment by
 // segment from the anchor/local tensor and from the rank-major passing slots.
 //
-// Kernel design (one workgroup = 4 waves = 128 query rows of one query head):
+// Kernel design (one workgroup = 8 waves = 256 query rows of one query head):
 //  * Each wave owns 32 query rows and computes S^T = K Q^T with
 //    v_mfma_f32_32x32x16_bf16 (keys on the M side, queries on the N side).
 //    In that accumulator layout a lane holds one query and 16 keys, so the
-//    softmax row statistics are lane-local up to one exchange with the lane
-//    32 apart, and the probabilities are already laid out as the B operand of
+//    softmax row statistics are lane-local up to one v_permlane32_swap, and
+//    the probabilities are already laid out as the B operand of
 //    O^T = V^T P^T: no LDS round trip for P.
-//  * Q stays in registers for the whole key loop; K tiles (64 keys) are stored
-//    row-major in LDS, V tiles transposed, with the 64 keys of a tile permuted
-//    so that the 8 keys one lane contracts are contiguous (one 16-byte LDS
-//    read per MFMA operand).  Both tiles are double-buffered: the global loads
-//    of tile t+1 are in flight while tile t is computed.
+//  * Ping-pong: waves 0-3 (group A) and 4-7 (group B) put one wave on each
+//    SIMD.  The key loop runs in phases separated by workgroup barriers; in
+//    every phase one group issues its MFMAs (S(t) = K(t) Q^T and
+//    O += P(t-1) V(t-1)) while the other group runs the softmax of its last
+//    tile on the VALU, and the groups swap roles each phase, so each SIMD's
+//    MFMA pipe is fed by one wave while the other wave's exp/FMA work
+//    overlaps it.
+//  * K and V tiles (64 keys) sit row-major in LDS with an XOR swizzle of
+//    their 16-byte chunks: the K operand reads (ds_read_b128) and the
+//    transposing V operand reads (ds_read_b64_tr_b16) are both free of bank
+//    conflicts.  Tiles are double-buffered; all 8 waves stage the next tile
+//    through a few registers, loaded one phase before they are stored.
 //  * Online softmax in fp32 registers in base 2 (scale*log2(e) folded into one
 //    FMA), probabilities rounded to bf16 for the PV product, fp32 accumulate.
+//    The running max moves lazily (only when it grows by more than 2^8), so
+//    the O rescale is off the common path.
 //  * Tile classes per wave: key tiles wholly visible to all 32 rows run with
 //    no mask, tiles crossing the diagonal are masked element-wise, tiles
 //    beyond every row's visible prefix are skipped.
-//  * Running max updated lazily (only when it grows by more than 2^8), so
-//    the O rescale is off the common path.
 //  * Grid order puts the query tiles with the longest key prefix first, and
 //    keeps a GQA group's workgroups on one XCD (one L2) when n_kv % 8 == 0.
-//  * __launch_bounds__(256, 2): at most 256 VGPRs, two waves per SIMD, so one
-//    wave's softmax overlaps the other wave's MFMAs.
 #include <math.h>
 
 #include "apb_internal.h"
@@ -40,11 +45,19 @@ namespace apb {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr int kBM = 128;         // query rows per workgroup
-constexpr int kBN = 64;          // keys per tile
-constexpr int kThreads = 256;    // 4 waves
+constexpr int kWaves = 8;                   // two groups of one wave per SIMD
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRowsPerWave = 32;
+constexpr int kBM = kRowsPerWave * kWaves;  // query rows per workgroup
+constexpr int kBN = 64;                     // keys per tile
+constexpr int kXcds = 8;                    // MI355X: 8 XCDs, workgroups dealt round-robin
+constexpr float kRescaleSlack = 8.f;        // lazy rescale threshold, base-2 units
 
 struct Params {
   const uint16_t* q;
@@ -60,8 +73,9 @@ struct Params {
   float scale_log2;
 };
 
-constexpr int kXcds = 8;           // MI355X: 8 XCDs, workgroups dealt round-robin
-constexpr float kRescaleSlack = 8.f;  // lazy rescale threshold, base-2 units
+__device__ __forceinline__ int vis_end(int r, int La, int Lp) {
+  return (r < La ? r : r + Lp) + 1;
+}
 
 // Workgroup -> (query head, query tile).  Tiles with the longest key prefix
 // go first.  With xcd_map, consecutive workgroup ids land on different XCDs,
@@ -81,10 +95,6 @@ __device__ __forceinline__ void map_block(const Params& p, int bid, int& head, i
   }
 }
 
-__device__ __forceinline__ int vis_end(int r, int La, int Lp) {
-  return (r < La ? r : r + Lp) + 1;
-}
-
 // Address of concatenated key row c (0 <= c < Ktot) of KV head kvh.
 template <int D>
 __device__ __forceinline__ const uint16_t* key_row(const Params& p, const uint16_t* loc,
@@ -99,6 +109,24 @@ __device__ __forceinline__ const uint16_t* key_row(const Params& p, const uint16
   return loc + ((size_t)kvh * p.M + (c - p.Lp)) * D;
 }
 
+// Base address of key tile [c0, c0 + kBN) when it lies inside one segment
+// (anchor, one passing slot, or the local block) and below Ktot; nullptr
+// when the tile straddles a boundary and rows must be looked up one by one.
+template <int D>
+__device__ __forceinline__ const uint16_t* tile_base(const Params& p, const uint16_t* loc,
+                                                     const uint16_t* pass, int kvh, int c0) {
+  if (c0 + kBN > p.Ktot) return nullptr;
+  if (c0 + kBN <= p.La) return loc + ((size_t)kvh * p.M + c0) * D;
+  if (c0 >= p.La + p.Lp) return loc + ((size_t)kvh * p.M + (c0 - p.Lp)) * D;
+  if (c0 >= p.La && c0 + kBN <= p.La + p.Lp) {
+    const int t = c0 - p.La;
+    const int s = t / p.lp;
+    const int r = t - s * p.lp;
+    if (r + kBN <= p.lp) return pass + (((size_t)s * p.n_kv + kvh) * p.lp + r) * D;
+  }
+  return nullptr;
+}
+
 // Value held by the lane 32 apart (the other half of the wave holds the
 // other 16 keys of the same query in the 32x32 accumulator layout).
 __device__ __forceinline__ float half_swap(float x) {
@@ -108,35 +136,41 @@ __device__ __forceinline__ float half_swap(float x) {
   return __uint_as_float(lane < 32 ? r[1] : r[0]);
 }
 
-// Position of key kk (0..63) of a tile inside a transposed V row: the keys a
-// lane-half contracts in one 16-key MFMA step become 8 contiguous entries.
-__device__ __forceinline__ int vt_pos(int kk) {
-  const int sb = kk >> 5, qq = (kk >> 3) & 3, hh = (kk >> 2) & 1, i = kk & 3;
-  return 32 * sb + 16 * (qq >> 1) + 8 * hh + 4 * (qq & 1) + i;
+// LDS tile layouts: row-major [kBN][D] bf16, 16-byte chunk c of row r stored
+// at chunk position c ^ swz(r).
+//  K: swz = r mod (D/8): the 16 rows one ds_read_b128 pass touches hit 16
+//     different chunk positions.
+//  V: swz = 4 * (r mod 4) (D = 128): a transposing read touches 4 rows x 4
+//     chunks, which land on 16 different chunk positions.
+template <int D>
+__device__ __forceinline__ int k_swz(int r) { return r & (D / 8 - 1); }
+template <int D>
+__device__ __forceinline__ int v_swz(int r) { return (4 * (r & 3)) & (D / 8 - 1); }
+
+// Wait for this wave's outstanding LDS operations, then the workgroup
+// barrier.  Outstanding global loads are not waited for: the staged
+// registers carry their own dependency into the LDS stores.
+__device__ __forceinline__ void phase_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int D>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(kThreads)
 attn_fwd_kernel(Params p) {
-  constexpr int KST = D + 8;            // K tile row stride (bf16 elements)
-  constexpr int VST = kBN + 8;          // V^T tile row stride
-  constexpr int KCH = D / 8;            // 16-byte pieces per key row
-  constexpr int K_LOADS = kBN * KCH / kThreads;          // per thread
-  // V is staged in (4 keys x 8 dims) groups; consecutive lanes take
-  // consecutive key groups of one 8-dim chunk, so the transposed 8-byte LDS
-  // stores of 16 lanes hit 16 different bank pairs.
-  constexpr int V_GROUPS = (kBN / 4) * KCH;
-  constexpr int V_LOADS = (V_GROUPS + kThreads - 1) / kThreads;
-  constexpr int NKC = D / 16;           // MFMA k-steps over head_dim
-  constexpr int NDB = D / 32;           // 32-wide blocks of head_dim in O^T
-  static_assert(K_LOADS * kThreads == kBN * KCH, "K tile split");
+  constexpr int KCH = D / 8;                    // 16-byte chunks per key row
+  constexpr int TILE_CHUNKS = kBN * KCH;
+  constexpr int LOADS = TILE_CHUNKS / kThreads;  // per thread per tensor
+  constexpr int NKC = D / 16;                   // MFMA k-steps over head_dim
+  constexpr int NDB = D / 32;                   // 32-wide blocks of head_dim in O^T
+  static_assert(LOADS * kThreads == TILE_CHUNKS, "tile split");
 
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kBN * KST];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[2][D * VST];
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kBN * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
+  const int grp = wave >> 2;  // 0: group A, 1: group B
 
   int head, qtile;
   map_block(p, blockIdx.x, head, qtile);
@@ -145,18 +179,19 @@ attn_fwd_kernel(Params p) {
   const int r_last = min(r0 + kBM, p.M) - 1;
   const int ntiles = (vis_end(r_last, p.La, p.Lp) + kBN - 1) / kBN;
 
-  const int w_first = r0 + 32 * wave;
+  const int w_first = r0 + kRowsPerWave * wave;
   const bool w_valid = w_first < p.M;
   const int w_lo = vis_end(w_first, p.La, p.Lp);
-  const int w_hi = vis_end(min(w_first + 31, p.M - 1), p.La, p.Lp);
-  const int rq = w_first + n;                       // this lane's query row
+  const int w_hi = vis_end(min(w_first + kRowsPerWave - 1, p.M - 1), p.La, p.Lp);
+  const int w_tiles = w_valid ? (w_hi + kBN - 1) / kBN : 0;
+  const int rq = w_first + n;  // this lane's query row
   const int rq_end = vis_end(rq, p.La, p.Lp);
 
   // Q^T operand: query rq, head_dim slice 16*kc + 8*h .. +7.
   bf16x8 qreg[NKC];
   {
     const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq, p.M - 1)) * D;
-    #pragma unroll
+#pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
       uint4 raw = rq < p.M ? *reinterpret_cast<const uint4*>(qrow + 16 * kc + 8 * h)
                            : make_uint4(0u, 0u, 0u, 0u);
@@ -165,208 +200,241 @@ attn_fwd_kernel(Params p) {
   }
 
   f32x16 oacc[NDB];
-  #pragma unroll
+#pragma unroll
   for (int db = 0; db < NDB; ++db)
-    #pragma unroll
+#pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+  f32x16 s[2];
+  bf16x8 pb[4];
   float m_run = -INFINITY;  // running max of scaled logits (base-2 units)
   float l_run = 0.f;        // this lane-half's share of the running sum
 
-  uint4 kbuf[K_LOADS];
-  uint4 vbuf[V_LOADS][4];
+  u32x4 kbuf[LOADS], vbuf[LOADS];  // staged 16-byte chunks of the next tiles
 
-  // Global -> register staging of key tile t.  A tile that lies inside one
-  // segment (anchor, one passing slot, or local block) and below Ktot takes a
-  // single base address; tiles straddling a boundary fall back to per-row
-  // segment lookup.
-  auto load_tile = [&](int t) {
+  // Global -> register staging of this thread's chunks of key tile t of K
+  // (kbuf) or V (vbuf).  Rows past Ktot repeat row Ktot-1: they are masked
+  // for every query.
+  auto row_ptr = [&](const uint16_t* base, const uint16_t* loc, const uint16_t* pass, int c0,
+                     int row) -> const uint16_t* {
+    return base != nullptr ? base + (size_t)row * D
+                           : key_row<D>(p, loc, pass, kvh, min(c0 + row, p.Ktot - 1));
+  };
+  auto load_k = [&](int t) {
     const int c0 = t * kBN;
-    const uint16_t* kbase = nullptr;
-    const uint16_t* vbase = nullptr;
-    if (c0 + kBN <= p.Ktot) {
-      if (c0 + kBN <= p.La) {
-        const size_t off = ((size_t)kvh * p.M + c0) * D;
-        kbase = p.k + off; vbase = p.v + off;
-      } else if (c0 >= p.La + p.Lp) {
-        const size_t off = ((size_t)kvh * p.M + (c0 - p.Lp)) * D;
-        kbase = p.k + off; vbase = p.v + off;
-      } else if (c0 >= p.La && c0 + kBN <= p.La + p.Lp) {
-        const int tt = c0 - p.La;
-        const int sl = tt / p.lp;
-        const int r = tt - sl * p.lp;
-        if (r + kBN <= p.lp) {
-          const size_t off = (((size_t)sl * p.n_kv + kvh) * p.lp + r) * D;
-          kbase = p.kp + off; vbase = p.vp + off;
-        }
-      }
-    }
-    if (kbase != nullptr) {
-      #pragma unroll
-      for (int i = 0; i < K_LOADS; ++i) {
-        const int e = tid + i * kThreads;
-        const int row = e / KCH, ch = e - row * KCH;
-        kbuf[i] = *reinterpret_cast<const uint4*>(kbase + (size_t)row * D + 8 * ch);
-      }
-      #pragma unroll
-      for (int i = 0; i < V_LOADS; ++i) {
-        const int e = tid + i * kThreads;
-        if (e < V_GROUPS) {
-          const int g = e % (kBN / 4), ch = e / (kBN / 4);
-          #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            vbuf[i][j] = *reinterpret_cast<const uint4*>(vbase + (size_t)(4 * g + j) * D + 8 * ch);
-        }
-      }
-      return;
-    }
-    #pragma unroll
-    for (int i = 0; i < K_LOADS; ++i) {
+    const uint16_t* base = tile_base<D>(p, p.k, p.kp, kvh, c0);
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
       const int e = tid + i * kThreads;
       const int row = e / KCH, ch = e - row * KCH;
-      const int c = c0 + row;
-      kbuf[i] = c < p.Ktot
-                    ? *reinterpret_cast<const uint4*>(key_row<D>(p, p.k, p.kp, kvh, c) + 8 * ch)
-                    : make_uint4(0u, 0u, 0u, 0u);
+      kbuf[i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.k, p.kp, c0, row) + 8 * ch);
     }
-    #pragma unroll
-    for (int i = 0; i < V_LOADS; ++i) {
+  };
+  auto load_v = [&](int t) {
+    const int c0 = t * kBN;
+    const uint16_t* base = tile_base<D>(p, p.v, p.vp, kvh, c0);
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
       const int e = tid + i * kThreads;
-      if (e < V_GROUPS) {
-        const int g = e % (kBN / 4), ch = e / (kBN / 4);
-        #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int c = c0 + 4 * g + j;
-          vbuf[i][j] = c < p.Ktot
-                           ? *reinterpret_cast<const uint4*>(key_row<D>(p, p.v, p.vp, kvh, c) + 8 * ch)
-                           : make_uint4(0u, 0u, 0u, 0u);
-        }
-      }
+      const int row = e / KCH, ch = e - row * KCH;
+      vbuf[i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.v, p.vp, c0, row) + 8 * ch);
+    }
+  };
+  auto store_k = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int e = tid + i * kThreads;
+      const int row = e / KCH, ch = e - row * KCH;
+      *reinterpret_cast<u32x4*>(&k_lds[buf][row * D + 8 * (ch ^ k_swz<D>(row))]) = kbuf[i];
+    }
+  };
+  auto store_v = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int e = tid + i * kThreads;
+      const int row = e / KCH, ch = e - row * KCH;
+      *reinterpret_cast<u32x4*>(&v_lds[buf][row * D + 8 * (ch ^ v_swz<D>(row))]) = vbuf[i];
     }
   };
 
-  auto store_tile = [&](int buf) {
-    #pragma unroll
-    for (int i = 0; i < K_LOADS; ++i) {
-      const int e = tid + i * kThreads;
-      const int row = e / KCH, ch = e - row * KCH;
-      *reinterpret_cast<uint4*>(&k_lds[buf][row * KST + 8 * ch]) = kbuf[i];
-    }
-    #pragma unroll
-    for (int i = 0; i < V_LOADS; ++i) {
-      const int e = tid + i * kThreads;
-      if (e < V_GROUPS) {
-        const int g = e % (kBN / 4), ch = e / (kBN / 4);
-        const int pos = vt_pos(4 * g);
-        const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vbuf[i][0]);
-        const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vbuf[i][1]);
-        const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vbuf[i][2]);
-        const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vbuf[i][3]);
-        #pragma unroll
-        for (int d2 = 0; d2 < 4; ++d2) {
-          // dims 8*ch + 2*d2 (low halves) and 8*ch + 2*d2 + 1 (high halves)
-          const uint32_t a0 = w0[d2], a1 = w1[d2], a2 = w2[d2], a3 = w3[d2];
-          uint2 lo, hi;
-          lo.x = __builtin_amdgcn_perm(a1, a0, 0x05040100u);
-          lo.y = __builtin_amdgcn_perm(a3, a2, 0x05040100u);
-          hi.x = __builtin_amdgcn_perm(a1, a0, 0x07060302u);
-          hi.y = __builtin_amdgcn_perm(a3, a2, 0x07060302u);
-          *reinterpret_cast<uint2*>(&vt_lds[buf][(8 * ch + 2 * d2) * VST + pos]) = lo;
-          *reinterpret_cast<uint2*>(&vt_lds[buf][(8 * ch + 2 * d2 + 1) * VST + pos]) = hi;
-        }
-      }
-    }
+  // MFMA phase of tile t: S(t) = K(t) Q^T (QK steps i = 0..2*NKC-1: k-step
+  // i/2, key block i%2) and O^T += V(t-1)^T P(t-1)^T (PV steps i: 16-key
+  // group i/NDB, dim block i%NDB).  Both streams are interleaved step by
+  // step and their LDS operands are read two steps ahead into rotating
+  // registers, so the LDS latency hides behind the MFMAs.
+  //
+  // PV operands: MFMA step c contracts the 16 keys whose probabilities pb[c]
+  // holds: lane half hh, slot j <-> key 16c + 8*(j/4) + 4*hh + j%4 (the S^T
+  // accumulator layout).  The A operand (dims x keys) comes from two
+  // transposing reads of 4 keys each: in a 16-lane group g, source lane sl
+  // addresses key row 16c + 8*rd + 4*(g/2) + sl/4 at dims
+  // 32*db + 16*(g%2) + 4*(sl%4) .. +3, and result lane i, slot j gets element
+  // i%4 of source lane 4j + i/4.
+  constexpr int NQK = 2 * NKC;   // QK MFMA steps per tile
+  constexpr int NPV = 4 * NDB;   // PV MFMA steps per tile
+  auto k_operand = [&](const uint16_t* kl, int i) -> bf16x8 {
+    const int kc = i >> 1, row = 32 * (i & 1) + n;
+    return *reinterpret_cast<const bf16x8*>(&kl[row * D + 8 * ((2 * kc + h) ^ k_swz<D>(row))]);
   };
-
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) load_tile(t + 1);
-    const int c0 = t * kBN;
-    if (w_valid && c0 < w_hi) {
-      const uint16_t* kl = k_lds[buf];
-      const uint16_t* vl = vt_lds[buf];
-      f32x16 s[2];
-      #pragma unroll
+  auto v_operand = [&](const uint16_t* vl, int i) -> bf16x8 {
+    const int c = i / NDB, db = i % NDB;
+    const int g = lane >> 4, sl = lane & 15;
+    i16x4 part[2];
+#pragma unroll
+    for (int rd = 0; rd < 2; ++rd) {
+      const int row = 16 * c + 8 * rd + 4 * (g >> 1) + (sl >> 2);
+      const int dim = 32 * db + 16 * (g & 1) + 4 * (sl & 3);
+      const uint16_t* addr = &vl[row * D + 8 * ((dim >> 3) ^ v_swz<D>(row)) + (dim & 7)];
+      part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
+    }
+    return __builtin_bit_cast(
+        bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  auto qk_step = [&](const bf16x8& a, int i) {
+    s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[i >> 1], s[i & 1], 0, 0, 0);
+  };
+  auto pv_step = [&](const bf16x8& a, int i) {
+    oacc[i % NDB] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[i / NDB], oacc[i % NDB], 0, 0, 0);
+  };
+  auto mfma_phase = [&](int t, bool do_qk, bool do_pv) {
+    const uint16_t* kl = k_lds[t & 1];
+    const uint16_t* vl = v_lds[(t + 1) & 1];  // V(t-1)
+    if (do_qk) {
+#pragma unroll
       for (int sb = 0; sb < 2; ++sb)
-        #pragma unroll
+#pragma unroll
         for (int r = 0; r < 16; ++r) s[sb][r] = 0.f;
-      #pragma unroll
-      for (int kc = 0; kc < NKC; ++kc) {
-        #pragma unroll
-        for (int sb = 0; sb < 2; ++sb) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8*>(&kl[(32 * sb + n) * KST + 16 * kc + 8 * h]);
-          s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kc], s[sb], 0, 0, 0);
+    }
+    if (do_qk && do_pv) {
+      static_assert(NQK == NPV, "QK and PV step counts match for d in {64, 128}");
+      bf16x8 ka[3], va[3];
+      ka[0] = k_operand(kl, 0); va[0] = v_operand(vl, 0);
+      ka[1] = k_operand(kl, 1); va[1] = v_operand(vl, 1);
+#pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        if (i + 2 < NQK) {
+          ka[(i + 2) % 3] = k_operand(kl, i + 2);
+          va[(i + 2) % 3] = v_operand(vl, i + 2);
         }
+        qk_step(ka[i % 3], i);
+        pv_step(va[i % 3], i);
       }
-      if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
-        #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-          #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int c = c0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (c >= rq_end) s[sb][r] = -INFINITY;
-          }
+    } else if (do_qk) {
+      bf16x8 ka[3];
+      ka[0] = k_operand(kl, 0);
+      ka[1] = k_operand(kl, 1);
+#pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        if (i + 2 < NQK) ka[(i + 2) % 3] = k_operand(kl, i + 2);
+        qk_step(ka[i % 3], i);
       }
-      float mx = -INFINITY;
-      #pragma unroll
+    } else if (do_pv) {
+      bf16x8 va[3];
+      va[0] = v_operand(vl, 0);
+      va[1] = v_operand(vl, 1);
+#pragma unroll
+      for (int i = 0; i < NPV; ++i) {
+        if (i + 2 < NPV) va[(i + 2) % 3] = v_operand(vl, i + 2);
+        pv_step(va[i % 3], i);
+      }
+    }
+  };
+
+  // Softmax of tile t: mask, running max, exp2, row sums, P -> bf16.
+  auto softmax = [&](int t) {
+    const int c0 = t * kBN;
+    if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
+#pragma unroll
       for (int sb = 0; sb < 2; ++sb)
-        #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[sb][r]);
-      mx = fmaxf(mx, half_swap(mx));
-      const float m_tile = mx * p.scale_log2;
-      // Lazy rescale: the running max m_run only moves when some row's tile
-      // max exceeds it by more than 2^kRescaleSlack, so exp2 arguments stay
-      // <= kRescaleSlack and O and l share the same (possibly stale) m_run;
-      // O / l and m_run*ln2 + ln(l) are unchanged by the choice of m_run.
-      if (__any(m_tile > m_run + kRescaleSlack)) {
-        const float m_new = fmaxf(m_run, m_tile);
-        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-        #pragma unroll
-        for (int db = 0; db < NDB; ++db)
-          #pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-      }
-      float rs = 0.f;
-      bf16x8 pb[4];
-      #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
-        #pragma unroll
+#pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
-          rs += e;
-          pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
-        }
-      l_run += rs;
-      #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8*>(&vl[(32 * db + n) * VST + 16 * c + 8 * h]);
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[c], oacc[db], 0, 0, 0);
+          const int c = c0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (c >= rq_end) s[sb][r] = -INFINITY;
         }
     }
-    if (t + 1 < ntiles) store_tile(buf ^ 1);
-    __syncthreads();
+    float mq[4];  // four independent max chains
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j >> 1][8 * (j & 1)], s[j >> 1][8 * (j & 1) + 1]);
+#pragma unroll
+    for (int r = 2; r < 8; ++r)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j >> 1][8 * (j & 1) + r]);
+    float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+    mx = fmaxf(mx, half_swap(mx));
+    const float m_tile = mx * p.scale_log2;
+    // Lazy rescale: m_run only moves when some row's tile max exceeds it by
+    // more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack and
+    // O and l share the same (possibly stale) m_run; O / l and
+    // m_run*ln2 + ln(l) do not depend on the choice of m_run.
+    if (__any(m_tile > m_run + kRescaleSlack)) {
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    }
+    float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
+        rs[r & 3] += e;
+        pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
+      }
+    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+  };
+
+  // Prologue: K(0) in LDS.
+  load_k(0);
+  store_k(0);
+  phase_barrier();
+
+  // Phase ph.  Loads: in phase 2t (t < ntiles) this thread's share of K(t+1)
+  // and V(t) goes to registers; at the end of phase 2t+1 it is stored into
+  // k_lds[(t+1)&1] (last read in phase 2t-1) and v_lds[t&1] (last read in
+  // phase 2t-1).  Compute: group A runs MFMA(t) = {QK(t), PV(t-1)} in phase
+  // 2t and softmax(t) in phase 2t+1; group B runs the same one phase later.
+  const int nphase = 2 * ntiles + 2;
+  for (int ph = 0; ph < nphase; ++ph) {
+    const int lt = ph >> 1;  // tile whose V (and the next K) this phase pair stages
+    if ((ph & 1) == 0 && lt < ntiles) {
+      if (lt + 1 < ntiles) load_k(lt + 1);
+      load_v(lt);
+    }
+    const int my = ph - grp;
+    if (my >= 0) {
+      const int t = my >> 1;
+      if ((my & 1) == 0) {
+        // MFMA issue of this wave wins arbitration over the softmax wave
+        // sharing its SIMD.
+        __builtin_amdgcn_s_setprio(1);
+        mfma_phase(t, t < w_tiles, t >= 1 && t - 1 < w_tiles);
+        __builtin_amdgcn_s_setprio(0);
+      } else if (t < w_tiles) {
+        softmax(t);
+      }
+    }
+    if ((ph & 1) == 1 && lt < ntiles) {
+      if (lt + 1 < ntiles) store_k((lt + 1) & 1);
+      store_v(lt & 1);
+    }
+    phase_barrier();
   }
 
   if (!w_valid || rq >= p.M) return;
   const float l_tot = l_run + half_swap(l_run);
   const float inv = 1.f / l_tot;
   uint16_t* orow = p.o + ((size_t)head * p.M + rq) * D;
-  #pragma unroll
+#pragma unroll
   for (int db = 0; db < NDB; ++db)
-    #pragma unroll
+#pragma unroll
     for (int g = 0; g < 4; ++g) {
-      typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
       bf16x4 w;
-      #pragma unroll
+#pragma unroll
       for (int i = 0; i < 4; ++i) w[i] = (__bf16)(oacc[db][4 * g + i] * inv);
       *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
     }
