@@ -9,32 +9,34 @@
 // concatenation is never materialised: key rows are fetched segment by
 // segment from the anchor/local tensor and from the rank-major passing slots.
 //
-// Kernel design (one workgroup = 8 waves = 256 query rows of one query head):
+// Kernel design (one workgroup = 4 waves = 128 query rows of one query head,
+// two workgroups per CU, so two independent waves share each SIMD):
 //  * Each wave owns 32 query rows and computes S^T = K Q^T with
 //    v_mfma_f32_32x32x16_bf16 (keys on the M side, queries on the N side).
 //    In that accumulator layout a lane holds one query and 16 keys, so the
 //    softmax row statistics are lane-local up to one v_permlane32_swap, and
 //    the probabilities are already laid out as the B operand of
 //    O^T = V^T P^T: no LDS round trip for P.
-//  * Ping-pong: waves 0-3 (group A) and 4-7 (group B) put one wave on each
-//    SIMD.  The key loop runs in phases separated by workgroup barriers; in
-//    every phase one group issues its MFMAs (S(t) = K(t) Q^T and
-//    O += P(t-1) V(t-1)) while the other group runs the softmax of its last
-//    tile on the VALU, and the groups swap roles each phase, so each SIMD's
-//    MFMA pipe is fed by one wave while the other wave's exp/FMA work
-//    overlaps it.
-//  * K and V tiles (64 keys) sit row-major in LDS with an XOR swizzle of
+//  * In-wave software pipeline over 32-key units: while the VALU runs the
+//    softmax of unit u, the same wave's MFMAs compute the logits of unit u+1
+//    and the PV product of unit u-1, the three streams interleaved step by
+//    step.  Logits and probabilities are double-buffered in registers.  On
+//    gfx950 one wave issues VALU work far slower than its MFMA pipe retires
+//    32x32x16 products, so the exp/FMA work has to overlap MFMAs inside the
+//    wave, not only across waves.
+//  * K and V tiles (32 keys) sit row-major in LDS with an XOR swizzle of
 //    their 16-byte chunks: the K operand reads (ds_read_b128) and the
 //    transposing V operand reads (ds_read_b64_tr_b16) are both free of bank
-//    conflicts.  Tiles are double-buffered; all 8 waves stage the next tile
-//    through a few registers, loaded one phase before they are stored.
+//    conflicts.  Tiles are double-buffered and staged through registers: the
+//    global loads of a unit's successors are issued at its start and stored
+//    at its end, one barrier per unit.
 //  * Online softmax in fp32 registers in base 2 (scale*log2(e) folded into one
 //    FMA), probabilities rounded to bf16 for the PV product, fp32 accumulate.
 //    The running max moves lazily (only when it grows by more than 2^8), so
 //    the O rescale is off the common path.
-//  * Tile classes per wave: key tiles wholly visible to all 32 rows run with
-//    no mask, tiles crossing the diagonal are masked element-wise, tiles
-//    beyond every row's visible prefix are skipped.
+//  * Unit classes per wave: units wholly visible to all 32 rows run with no
+//    mask, units crossing the diagonal are masked element-wise, units beyond
+//    every row's visible prefix are skipped.
 //  * Grid order puts the query tiles with the longest key prefix first, and
 //    keeps a GQA group's workgroups on one XCD (one L2) when n_kv % 8 == 0.
 #include <math.h>
@@ -51,11 +53,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr int kWaves = 8;                   // two groups of one wave per SIMD
+constexpr int kWaves = 4;                   // one wave per SIMD; two workgroups per CU
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
 constexpr int kBM = kRowsPerWave * kWaves;  // query rows per workgroup
-constexpr int kBN = 64;                     // keys per tile
+constexpr int kBN = 32;                     // keys per pipeline unit (one LDS tile)
 constexpr int kXcds = 8;                    // MI355X: 8 XCDs, workgroups dealt round-robin
 constexpr float kRescaleSlack = 8.f;        // lazy rescale threshold, base-2 units
 
@@ -154,23 +156,34 @@ __device__ __forceinline__ void phase_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+template <int N>
+struct Slot {
+  static constexpr int value = N;
+};
+
 template <int D>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kThreads, 2)
 attn_fwd_kernel(Params p) {
-  constexpr int KCH = D / 8;                    // 16-byte chunks per key row
+  constexpr int KCH = D / 8;                     // 16-byte chunks per key row
   constexpr int TILE_CHUNKS = kBN * KCH;
   constexpr int LOADS = TILE_CHUNKS / kThreads;  // per thread per tensor
-  constexpr int NKC = D / 16;                   // MFMA k-steps over head_dim
-  constexpr int NDB = D / 32;                   // 32-wide blocks of head_dim in O^T
+  constexpr int NKC = D / 16;                    // QK MFMA steps per unit (k over head_dim)
+  constexpr int NDB = D / 32;                    // 32-wide blocks of head_dim in O^T
+  constexpr int NPV = 2 * NDB;                   // PV MFMA steps per unit (2 x 16 keys)
+  constexpr int EPS = 16 / NKC;                  // softmax elements per interleaved step
   static_assert(LOADS * kThreads == TILE_CHUNKS, "tile split");
+  static_assert(NKC == NPV, "QK and PV step counts match for d in {64, 128}");
 
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kBN * D];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  // Wave index in a scalar register: every per-wave quantity below (row
+  // range, tile counts, the pipeline's stage predicates) is then uniform and
+  // its branches are scalar branches, not exec-masked ones.
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, h = lane >> 5;
-  const int grp = wave >> 2;  // 0: group A, 1: group B
 
   int head, qtile;
   map_block(p, blockIdx.x, head, qtile);
@@ -185,7 +198,7 @@ attn_fwd_kernel(Params p) {
   const int w_hi = vis_end(min(w_first + kRowsPerWave - 1, p.M - 1), p.La, p.Lp);
   const int w_tiles = w_valid ? (w_hi + kBN - 1) / kBN : 0;
   const int rq = w_first + n;  // this lane's query row
-  const int rq_end = vis_end(rq, p.La, p.Lp);
+  const int rq_end = rq < p.M ? vis_end(rq, p.La, p.Lp) : 0;  // rows past M see nothing
 
   // Q^T operand: query rq, head_dim slice 16*kc + 8*h .. +7.
   bf16x8 qreg[NKC];
@@ -193,8 +206,8 @@ attn_fwd_kernel(Params p) {
     const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq, p.M - 1)) * D;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
-      uint4 raw = rq < p.M ? *reinterpret_cast<const uint4*>(qrow + 16 * kc + 8 * h)
-                           : make_uint4(0u, 0u, 0u, 0u);
+      u32x4 raw = rq < p.M ? *reinterpret_cast<const u32x4*>(qrow + 16 * kc + 8 * h)
+                           : u32x4{0u, 0u, 0u, 0u};
       qreg[kc] = __builtin_bit_cast(bf16x8, raw);
     }
   }
@@ -204,76 +217,74 @@ attn_fwd_kernel(Params p) {
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
-  f32x16 s[2];
-  bf16x8 pb[4];
+  f32x16 s[2];        // logits of units u (slot u&1) and u+1
+  bf16x8 pbuf[2][2];  // probabilities of units u (slot u&1) and u-1
   float m_run = -INFINITY;  // running max of scaled logits (base-2 units)
   float l_run = 0.f;        // this lane-half's share of the running sum
 
-  u32x4 kbuf[LOADS], vbuf[LOADS];  // staged 16-byte chunks of the next tiles
+  // Staged 16-byte chunks of upcoming tiles, two sets: the set loaded in unit
+  // u is stored to LDS at the end of unit u+1, so a global load has a whole
+  // unit of work to arrive.
+  u32x4 kbuf[2][LOADS], vbuf[2][LOADS];
 
   // Global -> register staging of this thread's chunks of key tile t of K
-  // (kbuf) or V (vbuf).  Rows past Ktot repeat row Ktot-1: they are masked
-  // for every query.
+  // or V.  Rows past Ktot repeat row Ktot-1: they are masked for every query.
   auto row_ptr = [&](const uint16_t* base, const uint16_t* loc, const uint16_t* pass, int c0,
                      int row) -> const uint16_t* {
     return base != nullptr ? base + (size_t)row * D
                            : key_row<D>(p, loc, pass, kvh, min(c0 + row, p.Ktot - 1));
   };
-  auto load_k = [&](int t) {
+  auto load_k = [&](int t, auto set) {
+    constexpr int ST = decltype(set)::value;
     const int c0 = t * kBN;
     const uint16_t* base = tile_base<D>(p, p.k, p.kp, kvh, c0);
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int e = tid + i * kThreads;
       const int row = e / KCH, ch = e - row * KCH;
-      kbuf[i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.k, p.kp, c0, row) + 8 * ch);
+      kbuf[ST][i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.k, p.kp, c0, row) + 8 * ch);
     }
   };
-  auto load_v = [&](int t) {
+  auto load_v = [&](int t, auto set) {
+    constexpr int ST = decltype(set)::value;
     const int c0 = t * kBN;
     const uint16_t* base = tile_base<D>(p, p.v, p.vp, kvh, c0);
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int e = tid + i * kThreads;
       const int row = e / KCH, ch = e - row * KCH;
-      vbuf[i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.v, p.vp, c0, row) + 8 * ch);
+      vbuf[ST][i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.v, p.vp, c0, row) + 8 * ch);
     }
   };
-  auto store_k = [&](int buf) {
+  auto store_k = [&](int buf, auto set) {
+    constexpr int ST = decltype(set)::value;
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int e = tid + i * kThreads;
       const int row = e / KCH, ch = e - row * KCH;
-      *reinterpret_cast<u32x4*>(&k_lds[buf][row * D + 8 * (ch ^ k_swz<D>(row))]) = kbuf[i];
+      *reinterpret_cast<u32x4*>(&k_lds[buf][row * D + 8 * (ch ^ k_swz<D>(row))]) = kbuf[ST][i];
     }
   };
-  auto store_v = [&](int buf) {
+  auto store_v = [&](int buf, auto set) {
+    constexpr int ST = decltype(set)::value;
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int e = tid + i * kThreads;
       const int row = e / KCH, ch = e - row * KCH;
-      *reinterpret_cast<u32x4*>(&v_lds[buf][row * D + 8 * (ch ^ v_swz<D>(row))]) = vbuf[i];
+      *reinterpret_cast<u32x4*>(&v_lds[buf][row * D + 8 * (ch ^ v_swz<D>(row))]) = vbuf[ST][i];
     }
   };
 
-  // MFMA phase of tile t: S(t) = K(t) Q^T (QK steps i = 0..2*NKC-1: k-step
-  // i/2, key block i%2) and O^T += V(t-1)^T P(t-1)^T (PV steps i: 16-key
-  // group i/NDB, dim block i%NDB).  Both streams are interleaved step by
-  // step and their LDS operands are read two steps ahead into rotating
-  // registers, so the LDS latency hides behind the MFMAs.
-  //
-  // PV operands: MFMA step c contracts the 16 keys whose probabilities pb[c]
-  // holds: lane half hh, slot j <-> key 16c + 8*(j/4) + 4*hh + j%4 (the S^T
-  // accumulator layout).  The A operand (dims x keys) comes from two
-  // transposing reads of 4 keys each: in a 16-lane group g, source lane sl
-  // addresses key row 16c + 8*rd + 4*(g/2) + sl/4 at dims
-  // 32*db + 16*(g%2) + 4*(sl%4) .. +3, and result lane i, slot j gets element
-  // i%4 of source lane 4j + i/4.
-  constexpr int NQK = 2 * NKC;   // QK MFMA steps per tile
-  constexpr int NPV = 4 * NDB;   // PV MFMA steps per tile
+  // LDS operands.  QK step i (k over head_dim 16i .. 16i+15): A = K rows
+  // (lane n holds key n of the unit).  PV step i: 16-key group c = i / NDB,
+  // dim block db = i % NDB; pbuf[.][c] slot j of lane half hh holds key
+  // 16c + 8*(j/4) + 4*hh + j%4 (the S^T accumulator layout), and the A operand
+  // (dims x keys) comes from two transposing reads of 4 keys each: in a
+  // 16-lane group g, source lane sl addresses key row 16c + 8*rd + 4*(g/2) +
+  // sl/4 at dims 32*db + 16*(g%2) + 4*(sl%4) .. +3, and result lane i, slot j
+  // gets element i%4 of source lane 4j + i/4.
   auto k_operand = [&](const uint16_t* kl, int i) -> bf16x8 {
-    const int kc = i >> 1, row = 32 * (i & 1) + n;
-    return *reinterpret_cast<const bf16x8*>(&kl[row * D + 8 * ((2 * kc + h) ^ k_swz<D>(row))]);
+    return *reinterpret_cast<const bf16x8*>(&kl[n * D + 8 * ((2 * i + h) ^ k_swz<D>(n))]);
   };
   auto v_operand = [&](const uint16_t* vl, int i) -> bf16x8 {
     const int c = i / NDB, db = i % NDB;
@@ -289,85 +300,52 @@ attn_fwd_kernel(Params p) {
     return __builtin_bit_cast(
         bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  auto qk_step = [&](const bf16x8& a, int i) {
-    s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[i >> 1], s[i & 1], 0, 0, 0);
-  };
-  auto pv_step = [&](const bf16x8& a, int i) {
-    oacc[i % NDB] =
-        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[i / NDB], oacc[i % NDB], 0, 0, 0);
-  };
-  auto mfma_phase = [&](int t, bool do_qk, bool do_pv) {
-    const uint16_t* kl = k_lds[t & 1];
-    const uint16_t* vl = v_lds[(t + 1) & 1];  // V(t-1)
-    if (do_qk) {
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[sb][r] = 0.f;
-    }
-    if (do_qk && do_pv) {
-      static_assert(NQK == NPV, "QK and PV step counts match for d in {64, 128}");
-      bf16x8 ka[3], va[3];
-      ka[0] = k_operand(kl, 0); va[0] = v_operand(vl, 0);
-      ka[1] = k_operand(kl, 1); va[1] = v_operand(vl, 1);
-#pragma unroll
-      for (int i = 0; i < NQK; ++i) {
-        if (i + 2 < NQK) {
-          ka[(i + 2) % 3] = k_operand(kl, i + 2);
-          va[(i + 2) % 3] = v_operand(vl, i + 2);
-        }
-        qk_step(ka[i % 3], i);
-        pv_step(va[i % 3], i);
-      }
-    } else if (do_qk) {
-      bf16x8 ka[3];
-      ka[0] = k_operand(kl, 0);
-      ka[1] = k_operand(kl, 1);
-#pragma unroll
-      for (int i = 0; i < NQK; ++i) {
-        if (i + 2 < NQK) ka[(i + 2) % 3] = k_operand(kl, i + 2);
-        qk_step(ka[i % 3], i);
-      }
-    } else if (do_pv) {
-      bf16x8 va[3];
-      va[0] = v_operand(vl, 0);
-      va[1] = v_operand(vl, 1);
-#pragma unroll
-      for (int i = 0; i < NPV; ++i) {
-        if (i + 2 < NPV) va[(i + 2) % 3] = v_operand(vl, i + 2);
-        pv_step(va[i % 3], i);
-      }
-    }
-  };
 
-  // Softmax of tile t: mask, running max, exp2, row sums, P -> bf16.
-  auto softmax = [&](int t) {
-    const int c0 = t * kBN;
-    if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
+  // One 32-key unit u of the pipeline: softmax of S_u (slot SL) interleaved
+  // with QK_{u+1} (into slot SL^1, K tile u+1) and, when WITH_PV, PV_{u-1}
+  // (probabilities in slot SL^1, V tile u-1).  Every stage runs for every
+  // unit: units past a wave's visible range are fully masked and contribute
+  // zeros, which keeps the body one straight-line block for the scheduler.
+  auto unit = [&](int u, auto slot, auto with_pv) {
+    constexpr int SL = decltype(slot)::value;
+    constexpr bool PV = decltype(with_pv)::value != 0;
+    if (u + 3 < ntiles) load_k(u + 3, Slot<SL>());
+    if (u + 1 < ntiles) load_v(u + 1, Slot<SL>());
+    const uint16_t* kl = k_lds[(u + 1) & 1];
+    const uint16_t* vl = v_lds[(u + 1) & 1];  // V tile u-1
+    // The first half of QK_{u+1} does not depend on this unit's softmax: its
+    // MFMAs run while the row max and the rescale test below are computed.
+    constexpr int NEARLY = NKC / 2;
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+    for (int r = 0; r < 16; ++r) s[SL ^ 1][r] = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int c = c0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (c >= rq_end) s[sb][r] = -INFINITY;
-        }
+    for (int i = 0; i < NEARLY; ++i)
+      s[SL ^ 1] =
+          __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_operand(kl, i), qreg[i], s[SL ^ 1], 0, 0, 0);
+    const int c0 = u * kBN;
+    if (c0 + kBN > w_lo) {  // unit crosses some row's visible end
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (c >= rq_end) s[SL][r] = -INFINITY;
+      }
     }
     float mq[4];  // four independent max chains
 #pragma unroll
-    for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j >> 1][8 * (j & 1)], s[j >> 1][8 * (j & 1) + 1]);
+    for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[SL][j], s[SL][j + 4]);
 #pragma unroll
-    for (int r = 2; r < 8; ++r)
+    for (int r = 8; r < 16; r += 4)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j >> 1][8 * (j & 1) + r]);
+      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[SL][r + j]);
     float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
     mx = fmaxf(mx, half_swap(mx));
-    const float m_tile = mx * p.scale_log2;
-    // Lazy rescale: m_run only moves when some row's tile max exceeds it by
+    const float m_blk = mx * p.scale_log2;
+    // Lazy rescale: m_run only moves when some row's unit max exceeds it by
     // more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack and
-    // O and l share the same (possibly stale) m_run; O / l and
-    // m_run*ln2 + ln(l) do not depend on the choice of m_run.
-    if (__any(m_tile > m_run + kRescaleSlack)) {
-      const float m_new = fmaxf(m_run, m_tile);
+    // O, l and the pending P_{u-1} share the same (possibly stale) m_run;
+    // O / l and m_run*ln2 + ln(l) do not depend on the choice.
+    if (__any(m_blk > m_run + kRescaleSlack)) {
+      const float m_new = fmaxf(m_run, m_blk);
       const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
       l_run *= alpha;
@@ -375,55 +353,80 @@ attn_fwd_kernel(Params p) {
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      if (PV) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            pbuf[SL ^ 1][c][j] = (__bf16)((float)pbuf[SL ^ 1][c][j] * alpha);
+      }
     }
     float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
+    // Remaining QK steps, PV steps and softmax steps interleaved; LDS
+    // operands two steps ahead in rotating registers.
+    bf16x8 ka[3], va[3];
+    ka[0] = k_operand(kl, NEARLY);
+    ka[1] = k_operand(kl, NEARLY + 1);
+    if (PV) {
+      va[0] = v_operand(vl, 0);
+      va[1] = v_operand(vl, 1);
+    }
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
-        rs[r & 3] += e;
-        pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
+    for (int i = 0; i < NKC; ++i) {
+      if (i + 2 < NKC) {
+        if (NEARLY + i + 2 < NKC) ka[(i + 2) % 3] = k_operand(kl, NEARLY + i + 2);
+        if (PV) va[(i + 2) % 3] = v_operand(vl, i + 2);
       }
+      if (NEARLY + i < NKC)
+        s[SL ^ 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qreg[NEARLY + i],
+                                                             s[SL ^ 1], 0, 0, 0);
+#pragma unroll
+      for (int x = 0; x < EPS; ++x) {  // softmax elements EPS*i .. EPS*i + EPS-1
+        const int r = EPS * i + x;
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[SL][r], p.scale_log2, -m_run));
+        rs[r & 3] += e;
+        pbuf[SL][r >> 3][r & 7] = (__bf16)e;
+      }
+      if (PV)
+        oacc[i % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            va[i % 3], pbuf[SL ^ 1][i / NDB], oacc[i % NDB], 0, 0, 0);
+    }
     l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+    // The set loaded in unit u-1 holds K(u+2) and V(u).  K(u+2) replaces
+    // K(u) (last read by QK_u in unit u-1); V(u) replaces V(u-2) (last read
+    // by PV_{u-2} in unit u-1).
+    if (u + 2 < ntiles) store_k(u & 1, Slot<SL ^ 1>());
+    if (u < ntiles) store_v(u & 1, Slot<SL ^ 1>());
+    phase_barrier();
   };
 
-  // Prologue: K(0) in LDS.
-  load_k(0);
-  store_k(0);
-  phase_barrier();
-
-  // Phase ph.  Loads: in phase 2t (t < ntiles) this thread's share of K(t+1)
-  // and V(t) goes to registers; at the end of phase 2t+1 it is stored into
-  // k_lds[(t+1)&1] (last read in phase 2t-1) and v_lds[t&1] (last read in
-  // phase 2t-1).  Compute: group A runs MFMA(t) = {QK(t), PV(t-1)} in phase
-  // 2t and softmax(t) in phase 2t+1; group B runs the same one phase later.
-  const int nphase = 2 * ntiles + 2;
-  for (int ph = 0; ph < nphase; ++ph) {
-    const int lt = ph >> 1;  // tile whose V (and the next K) this phase pair stages
-    if ((ph & 1) == 0 && lt < ntiles) {
-      if (lt + 1 < ntiles) load_k(lt + 1);
-      load_v(lt);
-    }
-    const int my = ph - grp;
-    if (my >= 0) {
-      const int t = my >> 1;
-      if ((my & 1) == 0) {
-        // MFMA issue of this wave wins arbitration over the softmax wave
-        // sharing its SIMD.
-        __builtin_amdgcn_s_setprio(1);
-        mfma_phase(t, t < w_tiles, t >= 1 && t - 1 < w_tiles);
-        __builtin_amdgcn_s_setprio(0);
-      } else if (t < w_tiles) {
-        softmax(t);
-      }
-    }
-    if ((ph & 1) == 1 && lt < ntiles) {
-      if (lt + 1 < ntiles) store_k((lt + 1) & 1);
-      store_v(lt & 1);
-    }
-    phase_barrier();
+  // Prologue: K tiles 0 and 1 in LDS, K(2) and V(0) staged in set 1 for
+  // unit 0, S_0 = K(0) Q^T.
+  load_k(0, Slot<0>());
+  store_k(0, Slot<0>());
+  if (ntiles > 1) {
+    load_k(1, Slot<0>());
+    store_k(1, Slot<0>());
   }
+  if (ntiles > 2) load_k(2, Slot<1>());
+  load_v(0, Slot<1>());
+  phase_barrier();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) s[0][r] = 0.f;
+#pragma unroll
+  for (int i = 0; i < NKC; ++i)
+    s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_operand(k_lds[0], i), qreg[i], s[0], 0, 0,
+                                                   0);
+  phase_barrier();  // unit 0 overwrites K(0)
+  // Units 0 .. ntiles: unit 0 has no PV yet, unit ntiles only finishes the
+  // last PV.
+  unit(0, Slot<0>(), Slot<0>());
+  int u = 1;
+  for (; u + 1 <= ntiles; u += 2) {
+    unit(u, Slot<1>(), Slot<1>());
+    unit(u + 1, Slot<0>(), Slot<1>());
+  }
+  if (u <= ntiles) unit(u, Slot<1>(), Slot<1>());
 
   if (!w_valid || rq >= p.M) return;
   const float l_tot = l_run + half_swap(l_run);
