@@ -57,7 +57,16 @@ constexpr int kWaves = 4;                   // one wave per SIMD; two workgroups
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
 constexpr int kBM = kRowsPerWave * kWaves;  // query rows per workgroup
-constexpr int kBN = 32;                     // keys per pipeline unit (one LDS tile)
+constexpr int kBN = 32;                     // keys per tile
+#ifndef APB_WAVES_PER_SIMD
+#define APB_WAVES_PER_SIMD 2
+#endif
+#ifndef APB_STAGES
+#define APB_STAGES 3
+#endif
+constexpr int kWavesPerSimd = APB_WAVES_PER_SIMD;  // occupancy target (VGPR budget)
+constexpr int kStages = APB_STAGES;                // LDS ring depth for K and V tiles
+constexpr int kAhead = kStages - 1;                // tiles in flight ahead of the one computed
 constexpr int kXcds = 8;                    // MI355X: 8 XCDs, workgroups dealt round-robin
 constexpr float kRescaleSlack = 8.f;        // lazy rescale threshold, base-2 units
 
@@ -149,6 +158,11 @@ __device__ __forceinline__ int k_swz(int r) { return r & (D / 8 - 1); }
 template <int D>
 __device__ __forceinline__ int v_swz(int r) { return (4 * (r & 3)) & (D / 8 - 1); }
 
+// Byte offset of an LDS location, as M0 and LDS instructions address it.
+__device__ __forceinline__ uint32_t lds_offset(const uint16_t* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint16_t*)p;
+}
+
 // Wait for this wave's outstanding LDS operations, then the workgroup
 // barrier.  Outstanding global loads are not waited for: the staged
 // registers carry their own dependency into the LDS stores.
@@ -156,32 +170,25 @@ __device__ __forceinline__ void phase_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int N>
-struct Slot {
-  static constexpr int value = N;
-};
-
 template <int D>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(kThreads, kWavesPerSimd)
 attn_fwd_kernel(Params p) {
   constexpr int KCH = D / 8;                     // 16-byte chunks per key row
-  constexpr int TILE_CHUNKS = kBN * KCH;
-  constexpr int LOADS = TILE_CHUNKS / kThreads;  // per thread per tensor
-  constexpr int NKC = D / 16;                    // QK MFMA steps per unit (k over head_dim)
+  constexpr int PIECE_ELEMS = 512;               // one 1 KiB DMA piece, in bf16
+  constexpr int ROWS_PER_PIECE = PIECE_ELEMS / D;
+  constexpr int DMA_PER_WAVE = kBN * D / PIECE_ELEMS / kWaves;  // pieces per wave per tensor
+  constexpr int NKC = D / 16;                    // QK MFMA steps per tile (k over head_dim)
   constexpr int NDB = D / 32;                    // 32-wide blocks of head_dim in O^T
-  constexpr int NPV = 2 * NDB;                   // PV MFMA steps per unit (2 x 16 keys)
-  constexpr int EPS = 16 / NKC;                  // softmax elements per interleaved step
-  static_assert(LOADS * kThreads == TILE_CHUNKS, "tile split");
-  static_assert(NKC == NPV, "QK and PV step counts match for d in {64, 128}");
+  static_assert(DMA_PER_WAVE * kWaves * PIECE_ELEMS == kBN * D, "tile split");
+  static_assert(DMA_PER_WAVE == 1 || DMA_PER_WAVE == 2, "vmcnt immediates below");
 
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kStages][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kStages][kBN * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // Wave index in a scalar register: every per-wave quantity below (row
-  // range, tile counts, the pipeline's stage predicates) is then uniform and
-  // its branches are scalar branches, not exec-masked ones.
+  // range, tile counts) is uniform and its branches are scalar branches.
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, h = lane >> 5;
 
@@ -198,7 +205,7 @@ attn_fwd_kernel(Params p) {
   const int w_hi = vis_end(min(w_first + kRowsPerWave - 1, p.M - 1), p.La, p.Lp);
   const int w_tiles = w_valid ? (w_hi + kBN - 1) / kBN : 0;
   const int rq = w_first + n;  // this lane's query row
-  const int rq_end = rq < p.M ? vis_end(rq, p.La, p.Lp) : 0;  // rows past M see nothing
+  const int rq_end = vis_end(rq, p.La, p.Lp);
 
   // Q^T operand: query rq, head_dim slice 16*kc + 8*h .. +7.
   bf16x8 qreg[NKC];
@@ -217,67 +224,75 @@ attn_fwd_kernel(Params p) {
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
-  f32x16 s[2];        // logits of units u (slot u&1) and u+1
-  bf16x8 pbuf[2][2];  // probabilities of units u (slot u&1) and u-1
   float m_run = -INFINITY;  // running max of scaled logits (base-2 units)
   float l_run = 0.f;        // this lane-half's share of the running sum
 
-  // Staged 16-byte chunks of upcoming tiles, two sets: the set loaded in unit
-  // u is stored to LDS at the end of unit u+1, so a global load has a whole
-  // unit of work to arrive.
-  u32x4 kbuf[2][LOADS], vbuf[2][LOADS];
-
-  // Global -> register staging of this thread's chunks of key tile t of K
-  // or V.  Rows past Ktot repeat row Ktot-1: they are masked for every query.
-  auto row_ptr = [&](const uint16_t* base, const uint16_t* loc, const uint16_t* pass, int c0,
-                     int row) -> const uint16_t* {
-    return base != nullptr ? base + (size_t)row * D
-                           : key_row<D>(p, loc, pass, kvh, min(c0 + row, p.Ktot - 1));
-  };
-  auto load_k = [&](int t, auto set) {
-    constexpr int ST = decltype(set)::value;
+  // HBM -> LDS copies of key tile t (K and V) straight into LDS stage st,
+  // without registers: global_load_lds_dwordx4 writes the 16 bytes of lane
+  // l to LDS address M0 + 16*l, so each instruction fills one 1 KiB piece of
+  // the swizzled tile and every lane fetches the chunk that belongs at its
+  // slot.  Each wave issues DMA_PER_WAVE such instructions per tensor.  For a
+  // tile inside one segment the per-lane byte offsets within the tile are
+  // fixed (precomputed below) and only the tile base, a scalar, changes.
+  // Rows past Ktot repeat row Ktot-1: they are masked for every query.
+  uint32_t koff[DMA_PER_WAVE], voff[DMA_PER_WAVE];
+#pragma unroll
+  for (int j = 0; j < DMA_PER_WAVE; ++j) {
+    const int row = (wave * DMA_PER_WAVE + j) * ROWS_PER_PIECE + lane / KCH;
+    const int slot = lane % KCH;
+    koff[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ k_swz<D>(row)));
+    voff[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ v_swz<D>(row)));
+  }
+  auto dma_tile = [&](int t, int st) {
     const int c0 = t * kBN;
-    const uint16_t* base = tile_base<D>(p, p.k, p.kp, kvh, c0);
+    const uint16_t* kb = tile_base<D>(p, p.k, p.kp, kvh, c0);
+    const uint16_t* vb = tile_base<D>(p, p.v, p.vp, kvh, c0);
+    if (kb != nullptr) {
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int e = tid + i * kThreads;
-      const int row = e / KCH, ch = e - row * KCH;
-      kbuf[ST][i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.k, p.kp, c0, row) + 8 * ch);
+      for (int j = 0; j < DMA_PER_WAVE; ++j) {
+        const int piece = wave * DMA_PER_WAVE + j;
+        const uint32_t kdst = lds_offset(&k_lds[st][piece * PIECE_ELEMS]);
+        const uint32_t vdst = lds_offset(&v_lds[st][piece * PIECE_ELEMS]);
+        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(koff[j]),
+                     "s"(kb), "s"(kdst)
+                     : "memory");
+        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff[j]),
+                     "s"(vb), "s"(vdst)
+                     : "memory");
+      }
+      return;
+    }
+#pragma unroll
+    for (int j = 0; j < DMA_PER_WAVE; ++j) {
+      const int piece = wave * DMA_PER_WAVE + j;
+      const int row = piece * ROWS_PER_PIECE + lane / KCH;
+      const int slot = lane % KCH;
+      const int c = min(c0 + row, p.Ktot - 1);
+      const uint16_t* ksrc = key_row<D>(p, p.k, p.kp, kvh, c) + 8 * (slot ^ k_swz<D>(row));
+      const uint16_t* vsrc = key_row<D>(p, p.v, p.vp, kvh, c) + 8 * (slot ^ v_swz<D>(row));
+      const uint32_t kdst = lds_offset(&k_lds[st][piece * PIECE_ELEMS]);
+      const uint32_t vdst = lds_offset(&v_lds[st][piece * PIECE_ELEMS]);
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(ksrc), "s"(kdst)
+                   : "memory");
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(vsrc), "s"(vdst)
+                   : "memory");
     }
   };
-  auto load_v = [&](int t, auto set) {
-    constexpr int ST = decltype(set)::value;
-    const int c0 = t * kBN;
-    const uint16_t* base = tile_base<D>(p, p.v, p.vp, kvh, c0);
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int e = tid + i * kThreads;
-      const int row = e / KCH, ch = e - row * KCH;
-      vbuf[ST][i] = *reinterpret_cast<const u32x4*>(row_ptr(base, p.v, p.vp, c0, row) + 8 * ch);
-    }
-  };
-  auto store_k = [&](int buf, auto set) {
-    constexpr int ST = decltype(set)::value;
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int e = tid + i * kThreads;
-      const int row = e / KCH, ch = e - row * KCH;
-      *reinterpret_cast<u32x4*>(&k_lds[buf][row * D + 8 * (ch ^ k_swz<D>(row))]) = kbuf[ST][i];
-    }
-  };
-  auto store_v = [&](int buf, auto set) {
-    constexpr int ST = decltype(set)::value;
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int e = tid + i * kThreads;
-      const int row = e / KCH, ch = e - row * KCH;
-      *reinterpret_cast<u32x4*>(&v_lds[buf][row * D + 8 * (ch ^ v_swz<D>(row))]) = vbuf[ST][i];
-    }
+  // Wait until this wave's copies of the tile issued before the most recent
+  // one have landed (`newer_issued`: whether a later tile's copies follow).
+  // `newer` = number of later tiles whose copies are already in flight.
+  auto dma_wait = [&](int newer) {
+    const int n = newer * 2 * DMA_PER_WAVE;
+    if (n >= 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else if (n >= 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
+    else if (n >= 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else if (n >= 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
 
   // LDS operands.  QK step i (k over head_dim 16i .. 16i+15): A = K rows
-  // (lane n holds key n of the unit).  PV step i: 16-key group c = i / NDB,
-  // dim block db = i % NDB; pbuf[.][c] slot j of lane half hh holds key
+  // (lane n holds key n of the tile).  PV step i: 16-key group c = i / NDB,
+  // dim block db = i % NDB; pb[c] slot j of lane half hh holds key
   // 16c + 8*(j/4) + 4*hh + j%4 (the S^T accumulator layout), and the A operand
   // (dims x keys) comes from two transposing reads of 4 keys each: in a
   // 16-lane group g, source lane sl addresses key row 16c + 8*rd + 4*(g/2) +
@@ -301,132 +316,80 @@ attn_fwd_kernel(Params p) {
         bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
   };
 
-  // One 32-key unit u of the pipeline: softmax of S_u (slot SL) interleaved
-  // with QK_{u+1} (into slot SL^1, K tile u+1) and, when WITH_PV, PV_{u-1}
-  // (probabilities in slot SL^1, V tile u-1).  Every stage runs for every
-  // unit: units past a wave's visible range are fully masked and contribute
-  // zeros, which keeps the body one straight-line block for the scheduler.
-  auto unit = [&](int u, auto slot, auto with_pv) {
-    constexpr int SL = decltype(slot)::value;
-    constexpr bool PV = decltype(with_pv)::value != 0;
-    if (u + 3 < ntiles) load_k(u + 3, Slot<SL>());
-    if (u + 1 < ntiles) load_v(u + 1, Slot<SL>());
-    const uint16_t* kl = k_lds[(u + 1) & 1];
-    const uint16_t* vl = v_lds[(u + 1) & 1];  // V tile u-1
-    // The first half of QK_{u+1} does not depend on this unit's softmax: its
-    // MFMAs run while the row max and the rescale test below are computed.
-    constexpr int NEARLY = NKC / 2;
+  // Ring of kStages LDS stages: tile t lives in stage t % kStages; the copies
+  // of tile t+kAhead are issued at the start of tile t into the stage of
+  // tile t-1 (every wave has passed the barrier that ended tile t-1), and
+  // tile t+1 must have landed before the barrier that ends tile t.
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s[SL ^ 1][r] = 0.f;
+  for (int a = 0; a < kAhead; ++a)
+    if (a < ntiles) dma_tile(a, a);
+  dma_wait(min(ntiles, kAhead) - 1);
+  phase_barrier();
+
+  int st = 0;  // stage of tile t
+  for (int t = 0; t < ntiles; ++t) {
+    if (t + kAhead < ntiles) dma_tile(t + kAhead, st == 0 ? kStages - 1 : st - 1);
+    if (t < w_tiles) {
+      const uint16_t* kl = k_lds[st];
+      const uint16_t* vl = v_lds[st];
+      // S^T = K(t) Q^T: lane (n, h) holds keys 8*(r/4) + 4*h + r%4 of query n.
+      f32x16 s;
 #pragma unroll
-    for (int i = 0; i < NEARLY; ++i)
-      s[SL ^ 1] =
-          __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_operand(kl, i), qreg[i], s[SL ^ 1], 0, 0, 0);
-    const int c0 = u * kBN;
-    if (c0 + kBN > w_lo) {  // unit crosses some row's visible end
+      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+      for (int i = 0; i < NKC; ++i)
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_operand(kl, i), qreg[i], s, 0, 0, 0);
+      const int c0 = t * kBN;
+      if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (c >= rq_end) s[r] = -INFINITY;
+        }
+      }
+      float mq[4];  // four independent max chains
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j], s[j + 4]);
+#pragma unroll
+      for (int r = 8; r < 16; r += 4)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[r + j]);
+      float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+      mx = fmaxf(mx, half_swap(mx));
+      const float m_blk = mx * p.scale_log2;
+      // Lazy rescale: m_run only moves when some row's tile max exceeds it
+      // by more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack
+      // and O and l share the same (possibly stale) m_run; O / l and
+      // m_run*ln2 + ln(l) do not depend on the choice.
+      if (__any(m_blk > m_run + kRescaleSlack)) {
+        const float m_new = fmaxf(m_run, m_blk);
+        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      }
+      float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
+      bf16x8 pb[2];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (c >= rq_end) s[SL][r] = -INFINITY;
-      }
-    }
-    float mq[4];  // four independent max chains
-#pragma unroll
-    for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[SL][j], s[SL][j + 4]);
-#pragma unroll
-    for (int r = 8; r < 16; r += 4)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[SL][r + j]);
-    float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-    mx = fmaxf(mx, half_swap(mx));
-    const float m_blk = mx * p.scale_log2;
-    // Lazy rescale: m_run only moves when some row's unit max exceeds it by
-    // more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack and
-    // O, l and the pending P_{u-1} share the same (possibly stale) m_run;
-    // O / l and m_run*ln2 + ln(l) do not depend on the choice.
-    if (__any(m_blk > m_run + kRescaleSlack)) {
-      const float m_new = fmaxf(m_run, m_blk);
-      const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-      if (PV) {
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            pbuf[SL ^ 1][c][j] = (__bf16)((float)pbuf[SL ^ 1][c][j] * alpha);
-      }
-    }
-    float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
-    // Remaining QK steps, PV steps and softmax steps interleaved; LDS
-    // operands two steps ahead in rotating registers.
-    bf16x8 ka[3], va[3];
-    ka[0] = k_operand(kl, NEARLY);
-    ka[1] = k_operand(kl, NEARLY + 1);
-    if (PV) {
-      va[0] = v_operand(vl, 0);
-      va[1] = v_operand(vl, 1);
-    }
-#pragma unroll
-    for (int i = 0; i < NKC; ++i) {
-      if (i + 2 < NKC) {
-        if (NEARLY + i + 2 < NKC) ka[(i + 2) % 3] = k_operand(kl, NEARLY + i + 2);
-        if (PV) va[(i + 2) % 3] = v_operand(vl, i + 2);
-      }
-      if (NEARLY + i < NKC)
-        s[SL ^ 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qreg[NEARLY + i],
-                                                             s[SL ^ 1], 0, 0, 0);
-#pragma unroll
-      for (int x = 0; x < EPS; ++x) {  // softmax elements EPS*i .. EPS*i + EPS-1
-        const int r = EPS * i + x;
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[SL][r], p.scale_log2, -m_run));
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -m_run));
         rs[r & 3] += e;
-        pbuf[SL][r >> 3][r & 7] = (__bf16)e;
+        pb[r >> 3][r & 7] = (__bf16)e;
       }
-      if (PV)
-        oacc[i % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            va[i % 3], pbuf[SL ^ 1][i / NDB], oacc[i % NDB], 0, 0, 0);
+      l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+#pragma unroll
+      for (int i = 0; i < 2 * NDB; ++i)
+        oacc[i % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_operand(vl, i), pb[i / NDB],
+                                                               oacc[i % NDB], 0, 0, 0);
     }
-    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
-    // The set loaded in unit u-1 holds K(u+2) and V(u).  K(u+2) replaces
-    // K(u) (last read by QK_u in unit u-1); V(u) replaces V(u-2) (last read
-    // by PV_{u-2} in unit u-1).
-    if (u + 2 < ntiles) store_k(u & 1, Slot<SL ^ 1>());
-    if (u < ntiles) store_v(u & 1, Slot<SL ^ 1>());
+    // tile t+1 must have landed; copies of tiles t+2 .. t+kAhead may fly on
+    dma_wait(min(ntiles - 1 - (t + 1), kAhead - 1) < 0 ? 0 : min(ntiles - 1 - (t + 1), kAhead - 1));
     phase_barrier();
-  };
-
-  // Prologue: K tiles 0 and 1 in LDS, K(2) and V(0) staged in set 1 for
-  // unit 0, S_0 = K(0) Q^T.
-  load_k(0, Slot<0>());
-  store_k(0, Slot<0>());
-  if (ntiles > 1) {
-    load_k(1, Slot<0>());
-    store_k(1, Slot<0>());
+    st = st == kStages - 1 ? 0 : st + 1;
   }
-  if (ntiles > 2) load_k(2, Slot<1>());
-  load_v(0, Slot<1>());
-  phase_barrier();
-#pragma unroll
-  for (int r = 0; r < 16; ++r) s[0][r] = 0.f;
-#pragma unroll
-  for (int i = 0; i < NKC; ++i)
-    s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_operand(k_lds[0], i), qreg[i], s[0], 0, 0,
-                                                   0);
-  phase_barrier();  // unit 0 overwrites K(0)
-  // Units 0 .. ntiles: unit 0 has no PV yet, unit ntiles only finishes the
-  // last PV.
-  unit(0, Slot<0>(), Slot<0>());
-  int u = 1;
-  for (; u + 1 <= ntiles; u += 2) {
-    unit(u, Slot<1>(), Slot<1>());
-    unit(u + 1, Slot<0>(), Slot<1>());
-  }
-  if (u <= ntiles) unit(u, Slot<1>(), Slot<1>());
 
   if (!w_valid || rq >= p.M) return;
   const float l_tot = l_run + half_swap(l_run);
