@@ -55,11 +55,15 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kWaves = 4;                   // one wave per SIMD; two workgroups per CU
 constexpr int kThreads = 64 * kWaves;
-constexpr int kRowsPerWave = 32;
+#ifndef APB_ROW_BLOCKS
+#define APB_ROW_BLOCKS 1
+#endif
+constexpr int kRB = APB_ROW_BLOCKS;         // 32-row blocks per wave
+constexpr int kRowsPerWave = 32 * kRB;
 constexpr int kBM = kRowsPerWave * kWaves;  // query rows per workgroup
 constexpr int kBN = 32;                     // keys per tile
 #ifndef APB_WAVES_PER_SIMD
-#define APB_WAVES_PER_SIMD 2
+#define APB_WAVES_PER_SIMD (APB_ROW_BLOCKS == 1 ? 2 : 1)
 #endif
 #ifndef APB_STAGES
 #define APB_STAGES 3
@@ -204,28 +208,41 @@ attn_fwd_kernel(Params p) {
   const int w_lo = vis_end(w_first, p.La, p.Lp);
   const int w_hi = vis_end(min(w_first + kRowsPerWave - 1, p.M - 1), p.La, p.Lp);
   const int w_tiles = w_valid ? (w_hi + kBN - 1) / kBN : 0;
-  const int rq = w_first + n;  // this lane's query row
-  const int rq_end = vis_end(rq, p.La, p.Lp);
+  // Row block b of this wave covers rows w_first + 32*b .. +31; lane n of
+  // the S^T / O^T accumulators holds row w_first + 32*b + n.
+  int rq[kRB], rq_end[kRB];
+#pragma unroll
+  for (int b = 0; b < kRB; ++b) {
+    rq[b] = w_first + 32 * b + n;
+    rq_end[b] = vis_end(rq[b], p.La, p.Lp);
+  }
 
-  // Q^T operand: query rq, head_dim slice 16*kc + 8*h .. +7.
-  bf16x8 qreg[NKC];
-  {
-    const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq, p.M - 1)) * D;
+  // Q^T operands: query rq[b], head_dim slice 16*kc + 8*h .. +7.
+  bf16x8 qreg[kRB][NKC];
+#pragma unroll
+  for (int b = 0; b < kRB; ++b) {
+    const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq[b], p.M - 1)) * D;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
-      u32x4 raw = rq < p.M ? *reinterpret_cast<const u32x4*>(qrow + 16 * kc + 8 * h)
-                           : u32x4{0u, 0u, 0u, 0u};
-      qreg[kc] = __builtin_bit_cast(bf16x8, raw);
+      u32x4 raw = rq[b] < p.M ? *reinterpret_cast<const u32x4*>(qrow + 16 * kc + 8 * h)
+                              : u32x4{0u, 0u, 0u, 0u};
+      qreg[b][kc] = __builtin_bit_cast(bf16x8, raw);
     }
   }
 
-  f32x16 oacc[NDB];
+  f32x16 oacc[kRB][NDB];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int b = 0; b < kRB; ++b)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
-  float m_run = -INFINITY;  // running max of scaled logits (base-2 units)
-  float l_run = 0.f;        // this lane-half's share of the running sum
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[b][db][r] = 0.f;
+  float m_run[kRB], l_run[kRB];  // running max (base-2 units) and lane-half row sum
+#pragma unroll
+  for (int b = 0; b < kRB; ++b) {
+    m_run[b] = -INFINITY;
+    l_run[b] = 0.f;
+  }
 
   // HBM -> LDS copies of key tile t (K and V) straight into LDS stage st,
   // without registers: global_load_lds_dwordx4 writes the 16 bytes of lane
@@ -332,79 +349,109 @@ attn_fwd_kernel(Params p) {
     if (t < w_tiles) {
       const uint16_t* kl = k_lds[st];
       const uint16_t* vl = v_lds[st];
-      // S^T = K(t) Q^T: lane (n, h) holds keys 8*(r/4) + 4*h + r%4 of query n.
-      f32x16 s;
+      // S^T = K(t) Q^T per row block: lane (n, h) holds keys
+      // 8*(r/4) + 4*h + r%4 of query n.  Every K operand feeds kRB MFMAs.
+      f32x16 s[kRB];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+      for (int b = 0; b < kRB; ++b)
 #pragma unroll
-      for (int i = 0; i < NKC; ++i)
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_operand(kl, i), qreg[i], s, 0, 0, 0);
+        for (int r = 0; r < 16; ++r) s[b][r] = 0.f;
+#pragma unroll
+      for (int i = 0; i < NKC; ++i) {
+        const bf16x8 a = k_operand(kl, i);
+#pragma unroll
+        for (int b = 0; b < kRB; ++b)
+          s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[b][i], s[b], 0, 0, 0);
+      }
       const int c0 = t * kBN;
       if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (c >= rq_end) s[r] = -INFINITY;
-        }
+        for (int b = 0; b < kRB; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (c >= rq_end[b]) s[b][r] = -INFINITY;
+          }
       }
-      float mq[4];  // four independent max chains
+      float m_blk[kRB];
+      bool grow = false;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j], s[j + 4]);
+      for (int b = 0; b < kRB; ++b) {
+        float mq[4];  // four independent max chains
 #pragma unroll
-      for (int r = 8; r < 16; r += 4)
+        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[b][j], s[b][j + 4]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[r + j]);
-      float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-      mx = fmaxf(mx, half_swap(mx));
-      const float m_blk = mx * p.scale_log2;
+        for (int r = 8; r < 16; r += 4)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[b][r + j]);
+        float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+        mx = fmaxf(mx, half_swap(mx));
+        m_blk[b] = mx * p.scale_log2;
+        grow = grow || (m_blk[b] > m_run[b] + kRescaleSlack);
+      }
       // Lazy rescale: m_run only moves when some row's tile max exceeds it
       // by more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack
       // and O and l share the same (possibly stale) m_run; O / l and
       // m_run*ln2 + ln(l) do not depend on the choice.
-      if (__any(m_blk > m_run + kRescaleSlack)) {
-        const float m_new = fmaxf(m_run, m_blk);
-        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
+      if (__any(grow)) {
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
+        for (int b = 0; b < kRB; ++b) {
+          const float m_new = fmaxf(m_run[b], m_blk[b]);
+          const float alpha =
+              m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[b] - m_new);
+          m_run[b] = m_new;
+          l_run[b] *= alpha;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+          for (int db = 0; db < NDB; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[b][db][r] *= alpha;
+        }
       }
-      float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
-      bf16x8 pb[2];
+      bf16x8 pb[kRB][2];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -m_run));
-        rs[r & 3] += e;
-        pb[r >> 3][r & 7] = (__bf16)e;
+      for (int b = 0; b < kRB; ++b) {
+        float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = __builtin_amdgcn_exp2f(fmaf(s[b][r], p.scale_log2, -m_run[b]));
+          rs[r & 3] += e;
+          pb[b][r >> 3][r & 7] = (__bf16)e;
+        }
+        l_run[b] += (rs[0] + rs[1]) + (rs[2] + rs[3]);
       }
-      l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
 #pragma unroll
-      for (int i = 0; i < 2 * NDB; ++i)
-        oacc[i % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_operand(vl, i), pb[i / NDB],
-                                                               oacc[i % NDB], 0, 0, 0);
+      for (int i = 0; i < 2 * NDB; ++i) {  // every V operand feeds kRB MFMAs
+        const bf16x8 a = v_operand(vl, i);
+#pragma unroll
+        for (int b = 0; b < kRB; ++b)
+          oacc[b][i % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[b][i / NDB],
+                                                                    oacc[b][i % NDB], 0, 0, 0);
+      }
     }
-    // tile t+1 must have landed; copies of tiles t+2 .. t+kAhead may fly on
     dma_wait(min(ntiles - 1 - (t + 1), kAhead - 1) < 0 ? 0 : min(ntiles - 1 - (t + 1), kAhead - 1));
     phase_barrier();
     st = st == kStages - 1 ? 0 : st + 1;
   }
 
-  if (!w_valid || rq >= p.M) return;
-  const float l_tot = l_run + half_swap(l_run);
-  const float inv = 1.f / l_tot;
-  uint16_t* orow = p.o + ((size_t)head * p.M + rq) * D;
+  if (!w_valid) return;
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int b = 0; b < kRB; ++b) {
+    const float l_tot = l_run[b] + half_swap(l_run[b]);
+    if (rq[b] >= p.M) continue;
+    const float inv = 1.f / l_tot;
+    uint16_t* orow = p.o + ((size_t)head * p.M + rq[b]) * D;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      bf16x4 w;
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = (__bf16)(oacc[db][4 * g + i] * inv);
-      *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
-    }
-  if (p.lse && h == 0) p.lse[(size_t)head * p.M + rq] = m_run * 0.69314718055994531f + logf(l_tot);
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[i] = (__bf16)(oacc[b][db][4 * g + i] * inv);
+        *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
+      }
+    if (p.lse && h == 0)
+      p.lse[(size_t)head * p.M + rq[b]] = m_run[b] * 0.69314718055994531f + logf(l_tot);
+  }
 }
 
 }  // namespace
