@@ -9,34 +9,34 @@
 // concatenation is never materialised: key rows are fetched segment by
 // segment from the anchor/local tensor and from the rank-major passing slots.
 //
-// Kernel design (one workgroup = 4 waves = 128 query rows of one query head,
-// two workgroups per CU, so two independent waves share each SIMD):
+// Kernel design (one workgroup = 8 waves = 256 query rows of one query head,
+// one workgroup per CU):
 //  * Each wave owns 32 query rows and computes S^T = K Q^T with
 //    v_mfma_f32_32x32x16_bf16 (keys on the M side, queries on the N side).
-//    In that accumulator layout a lane holds one query and 16 keys, so the
-//    softmax row statistics are lane-local up to one v_permlane32_swap, and
-//    the probabilities are already laid out as the B operand of
-//    O^T = V^T P^T: no LDS round trip for P.
-//  * In-wave software pipeline over 32-key units: while the VALU runs the
-//    softmax of unit u, the same wave's MFMAs compute the logits of unit u+1
-//    and the PV product of unit u-1, the three streams interleaved step by
-//    step.  Logits and probabilities are double-buffered in registers.  On
-//    gfx950 one wave issues VALU work far slower than its MFMA pipe retires
-//    32x32x16 products, so the exp/FMA work has to overlap MFMAs inside the
-//    wave, not only across waves.
-//  * K and V tiles (32 keys) sit row-major in LDS with an XOR swizzle of
-//    their 16-byte chunks: the K operand reads (ds_read_b128) and the
-//    transposing V operand reads (ds_read_b64_tr_b16) are both free of bank
-//    conflicts.  Tiles are double-buffered and staged through registers: the
-//    global loads of a unit's successors are issued at its start and stored
-//    at its end, one barrier per unit.
+//    In that accumulator layout a lane holds one query and 16 keys of each
+//    32-key block, so the softmax row statistics are lane-local up to one
+//    v_permlane32_swap, and the probabilities are already laid out as the B
+//    operand of O^T = V^T P^T: no LDS round trip for P.
+//  * Ping-pong: the waves form two groups of four (one wave of each per
+//    SIMD) that alternate between an MFMA phase (S of the next 64-key tile
+//    and the PV product of the previous one, interleaved) and a softmax
+//    phase, the phases separated by workgroup barriers.  On every SIMD one
+//    wave feeds the matrix core while the other runs its exp/FMA work; a
+//    single wave cannot overlap the two on gfx950.
+//  * K and V tiles (64 keys) are copied HBM -> LDS by global_load_lds_dwordx4
+//    (no register staging) into a 4-stage ring; the copies ride in the
+//    softmax phases (K by one group, V by the other) and are waited for just
+//    before the barrier that opens the phase reading them, 3-4 phases later.
+//  * LDS tiles are row-major with an XOR swizzle of their 16-byte chunks: the
+//    K operand reads (ds_read_b128) and the transposing V operand reads
+//    (ds_read_b64_tr_b16) are free of bank conflicts, and each read address
+//    is one XOR of a per-lane base plus an immediate.
 //  * Online softmax in fp32 registers in base 2 (scale*log2(e) folded into one
 //    FMA), probabilities rounded to bf16 for the PV product, fp32 accumulate.
 //    The running max moves lazily (only when it grows by more than 2^8), so
 //    the O rescale is off the common path.
-//  * Unit classes per wave: units wholly visible to all 32 rows run with no
-//    mask, units crossing the diagonal are masked element-wise, units beyond
-//    every row's visible prefix are skipped.
+//  * Tiles crossing a row's visible end are masked element-wise; tiles past
+//    every row of the workgroup are not visited.
 //  * Grid order puts the query tiles with the longest key prefix first, and
 //    keeps a GQA group's workgroups on one XCD (one L2) when n_kv % 8 == 0.
 #include <math.h>
@@ -52,25 +52,18 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
-constexpr int kWaves = 4;                   // one wave per SIMD; two workgroups per CU
+constexpr int kGroupWaves = 4;                     // one wave per SIMD per group
+constexpr int kWaves = 2 * kGroupWaves;     // ping-pong groups A and B
 constexpr int kThreads = 64 * kWaves;
-#ifndef APB_ROW_BLOCKS
-#define APB_ROW_BLOCKS 1
-#endif
-constexpr int kRB = APB_ROW_BLOCKS;         // 32-row blocks per wave
-constexpr int kRowsPerWave = 32 * kRB;
+constexpr int kRowsPerWave = 32;
 constexpr int kBM = kRowsPerWave * kWaves;  // query rows per workgroup
-constexpr int kBN = 32;                     // keys per tile
-#ifndef APB_WAVES_PER_SIMD
-#define APB_WAVES_PER_SIMD (APB_ROW_BLOCKS == 1 ? 2 : 1)
+constexpr int kBN = 64;                            // keys per tile
+constexpr int kStages = 4;                         // LDS ring depth for K and V tiles
+#ifndef APB_PD
+#define APB_PD 2
 #endif
-#ifndef APB_STAGES
-#define APB_STAGES 3
-#endif
-constexpr int kWavesPerSimd = APB_WAVES_PER_SIMD;  // occupancy target (VGPR budget)
-constexpr int kStages = APB_STAGES;                // LDS ring depth for K and V tiles
-constexpr int kAhead = kStages - 1;                // tiles in flight ahead of the one computed
 constexpr int kXcds = 8;                    // MI355X: 8 XCDs, workgroups dealt round-robin
 constexpr float kRescaleSlack = 8.f;        // lazy rescale threshold, base-2 units
 
@@ -124,6 +117,20 @@ __device__ __forceinline__ const uint16_t* key_row(const Params& p, const uint16
   return loc + ((size_t)kvh * p.M + (c - p.Lp)) * D;
 }
 
+// key_row without branches (per-lane selects), for copies whose rows may
+// fall into different segments.
+template <int D>
+__device__ __forceinline__ const uint16_t* key_row_sel(const Params& p, const uint16_t* loc,
+                                                       const uint16_t* pass, int kvh, int c) {
+  const bool in_pass = c >= p.La && c < p.La + p.Lp;
+  const int t = in_pass ? c - p.La : 0;
+  const int s = t / p.lp;
+  const int r = t - s * p.lp;
+  const size_t pass_row = ((size_t)s * p.n_kv + kvh) * p.lp + r;
+  const size_t loc_row = (size_t)kvh * p.M + (c < p.La ? c : c - p.Lp);
+  return in_pass ? pass + pass_row * D : loc + loc_row * D;
+}
+
 // Base address of key tile [c0, c0 + kBN) when it lies inside one segment
 // (anchor, one passing slot, or the local block) and below Ktot; nullptr
 // when the tile straddles a boundary and rows must be looked up one by one.
@@ -167,33 +174,41 @@ __device__ __forceinline__ uint32_t lds_offset(const uint16_t* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint16_t*)p;
 }
 
-// Wait for this wave's outstanding LDS operations, then the workgroup
-// barrier.  Outstanding global loads are not waited for: the staged
-// registers carry their own dependency into the LDS stores.
+// Wait for this wave's outstanding LDS reads, then the workgroup barrier.
+// Outstanding HBM -> LDS copies are not waited for here: each copying wave
+// waits for its own copies (vmcnt) before the barrier that precedes their
+// first reader.
 __device__ __forceinline__ void phase_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int D>
-__global__ void __launch_bounds__(kThreads, kWavesPerSimd)
+__global__ void __launch_bounds__(kThreads, 1)
 attn_fwd_kernel(Params p) {
-  constexpr int KCH = D / 8;                     // 16-byte chunks per key row
   constexpr int PIECE_ELEMS = 512;               // one 1 KiB DMA piece, in bf16
   constexpr int ROWS_PER_PIECE = PIECE_ELEMS / D;
-  constexpr int DMA_PER_WAVE = kBN * D / PIECE_ELEMS / kWaves;  // pieces per wave per tensor
-  constexpr int NKC = D / 16;                    // QK MFMA steps per tile (k over head_dim)
+  constexpr int PIECES = kBN * D / PIECE_ELEMS;  // pieces per tile per tensor
+  constexpr int WP = PIECES / kGroupWaves;       // pieces per wave per tile
+  constexpr int KCH = D / 8;                     // 16-byte chunks per key row
+  constexpr int NKC = D / 16;                    // MFMA k-steps over head_dim
   constexpr int NDB = D / 32;                    // 32-wide blocks of head_dim in O^T
-  static_assert(DMA_PER_WAVE * kWaves * PIECE_ELEMS == kBN * D, "tile split");
-  static_assert(DMA_PER_WAVE == 1 || DMA_PER_WAVE == 2, "vmcnt immediates below");
+  constexpr int NQK = 2 * NKC;                   // QK MFMAs per tile (two 32-key blocks)
+  constexpr int NPV = 4 * NDB;                   // PV MFMAs per tile (four 16-key steps)
+  constexpr int PD = APB_PD;                     // LDS operand prefetch depth (MFMA steps)
+  static_assert(PIECES * PIECE_ELEMS == kBN * D && WP * kGroupWaves == PIECES, "tile split");
+  static_assert(WP == 2 || WP == 4, "vmcnt immediates below");
+  static_assert(NQK == NPV, "QK and PV step counts match for d in {64, 128}");
 
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kStages][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[kStages][kBN * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  // Wave index in a scalar register: every per-wave quantity below (row
-  // range, tile counts) is uniform and its branches are scalar branches.
+  // Wave index in a scalar register: every per-wave quantity below (group,
+  // row range, tile counts) is uniform and its branches are scalar branches.
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave / kGroupWaves;  // 0: group A, 1: group B
+  const int wig = wave % kGroupWaves;  // wave in group
   const int n = lane & 31, h = lane >> 5;
 
   int head, qtile;
@@ -203,255 +218,321 @@ attn_fwd_kernel(Params p) {
   const int r_last = min(r0 + kBM, p.M) - 1;
   const int ntiles = (vis_end(r_last, p.La, p.Lp) + kBN - 1) / kBN;
 
+  // Schedule, in phases separated by workgroup barriers.  Group A runs the
+  // MFMA step of tile t, {S(t) = K(t) Q^T, O += P(t-1) V(t-1)}, in phase 2t
+  // and the softmax of S(t) in phase 2t+1; group B runs the same one phase
+  // later, so on every SIMD one wave issues MFMAs while the other runs its
+  // exp/FMA work.  K(t) is read in phases 2t, 2t+1 and V(t) in 2t+2, 2t+3.
+  // The HBM -> LDS copies ride in the softmax phases: group B copies K(T) in
+  // phase 2T-4 and group A copies V(T) in phase 2T-3, both into ring stage
+  // T % kStages, whose previous tile was last read in phase 2T-5; each waits
+  // for its copy just before the barrier that opens the consuming phase.
+
+  // Copy lanes: global_load_lds_dwordx4 puts lane l's 16 bytes at M0 + 16*l,
+  // so each instruction fills one 1 KiB piece of the swizzled tile and every
+  // lane fetches the chunk that belongs at its slot.  The copies are inline
+  // asm so the compiler does not order the LDS operand reads behind them.
+  const bool copies_v = grp == 0;
+  const uint16_t* cp_loc = copies_v ? p.v : p.k;
+  const uint16_t* cp_pass = copies_v ? p.vp : p.kp;
+  uint32_t cp_off[WP];
+#pragma unroll
+  for (int j = 0; j < WP; ++j) {
+    const int row = (wig * WP + j) * ROWS_PER_PIECE + lane / KCH;
+    const int slot = lane % KCH;
+    const int swz = copies_v ? v_swz<D>(row) : k_swz<D>(row);
+    cp_off[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ swz));
+  }
+  auto issue = [&](int T) {
+    const int c0 = T * kBN;
+    const uint16_t* base = tile_base<D>(p, cp_loc, cp_pass, kvh, c0);
+    uint16_t* stage = copies_v ? v_lds[T % kStages] : k_lds[T % kStages];
+#pragma unroll
+    for (int j = 0; j < WP; ++j) {
+      const uint32_t dst = lds_offset(&stage[(wig * WP + j) * PIECE_ELEMS]);
+      if (base != nullptr) {
+        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(cp_off[j]),
+                     "s"(base), "s"(dst)
+                     : "memory", "m0");
+      } else {
+        const int row = (wig * WP + j) * ROWS_PER_PIECE + lane / KCH;
+        const int slot = lane % KCH;
+        const int c = min(c0 + row, p.Ktot - 1);
+        const int swz = copies_v ? v_swz<D>(row) : k_swz<D>(row);
+        const uint16_t* src = key_row_sel<D>(p, cp_loc, cp_pass, kvh, c) + 8 * (slot ^ swz);
+        asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst)
+                     : "memory", "m0");
+      }
+    }
+  };
+  // Wait until this wave's copies of tile T have landed, `later` of its
+  // copies of later tiles being allowed to stay in flight.
+  auto land = [&](int later) {
+    if (later >= 2) {
+      if constexpr (WP == 4) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    } else if (later == 1) {
+      if constexpr (WP == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+  };
+
   const int w_first = r0 + kRowsPerWave * wave;
   const bool w_valid = w_first < p.M;
-  const int w_lo = vis_end(w_first, p.La, p.Lp);
-  const int w_hi = vis_end(min(w_first + kRowsPerWave - 1, p.M - 1), p.La, p.Lp);
-  const int w_tiles = w_valid ? (w_hi + kBN - 1) / kBN : 0;
-  // Row block b of this wave covers rows w_first + 32*b .. +31; lane n of
-  // the S^T / O^T accumulators holds row w_first + 32*b + n.
-  int rq[kRB], rq_end[kRB];
-#pragma unroll
-  for (int b = 0; b < kRB; ++b) {
-    rq[b] = w_first + 32 * b + n;
-    rq_end[b] = vis_end(rq[b], p.La, p.Lp);
-  }
+  const int w_lo = vis_end(w_first, p.La, p.Lp);  // shortest visible prefix in the wave
+  const int rq = w_first + n;  // this lane's query row
+  const int rq_end = vis_end(rq, p.La, p.Lp);
 
-  // Q^T operands: query rq[b], head_dim slice 16*kc + 8*h .. +7.
-  bf16x8 qreg[kRB][NKC];
-#pragma unroll
-  for (int b = 0; b < kRB; ++b) {
-    const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq[b], p.M - 1)) * D;
+  // Q^T operand: query rq, head_dim slice 16*kc + 8*h .. +7.
+  bf16x8 qreg[NKC];
+  {
+    const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq, p.M - 1)) * D;
+    const unsigned keep = rq < p.M ? ~0u : 0u;  // rows past the end multiply by zero
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
-      u32x4 raw = rq[b] < p.M ? *reinterpret_cast<const u32x4*>(qrow + 16 * kc + 8 * h)
-                              : u32x4{0u, 0u, 0u, 0u};
-      qreg[b][kc] = __builtin_bit_cast(bf16x8, raw);
+      u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 16 * kc + 8 * h);
+      qreg[kc] = __builtin_bit_cast(bf16x8, raw & keep);
     }
   }
 
-  f32x16 oacc[kRB][NDB];
+  f32x16 oacc[NDB];
 #pragma unroll
-  for (int b = 0; b < kRB; ++b)
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[b][db][r] = 0.f;
-  float m_run[kRB], l_run[kRB];  // running max (base-2 units) and lane-half row sum
-#pragma unroll
-  for (int b = 0; b < kRB; ++b) {
-    m_run[b] = -INFINITY;
-    l_run[b] = 0.f;
-  }
+    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+  f32x16 s[2];   // S^T of the current tile: two 32-key blocks
+  bf16x8 pb[4];  // P of the previous tile: four 16-key MFMA steps
+  float m_run = -INFINITY;  // running max of scaled logits (base-2 units)
+  float l_run = 0.f;        // this lane-half's share of the running sum
 
-  // HBM -> LDS copies of key tile t (K and V) straight into LDS stage st,
-  // without registers: global_load_lds_dwordx4 writes the 16 bytes of lane
-  // l to LDS address M0 + 16*l, so each instruction fills one 1 KiB piece of
-  // the swizzled tile and every lane fetches the chunk that belongs at its
-  // slot.  Each wave issues DMA_PER_WAVE such instructions per tensor.  For a
-  // tile inside one segment the per-lane byte offsets within the tile are
-  // fixed (precomputed below) and only the tile base, a scalar, changes.
-  // Rows past Ktot repeat row Ktot-1: they are masked for every query.
-  uint32_t koff[DMA_PER_WAVE], voff[DMA_PER_WAVE];
-#pragma unroll
-  for (int j = 0; j < DMA_PER_WAVE; ++j) {
-    const int row = (wave * DMA_PER_WAVE + j) * ROWS_PER_PIECE + lane / KCH;
-    const int slot = lane % KCH;
-    koff[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ k_swz<D>(row)));
-    voff[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ v_swz<D>(row)));
-  }
-  auto dma_tile = [&](int t, int st) {
-    const int c0 = t * kBN;
-    const uint16_t* kb = tile_base<D>(p, p.k, p.kp, kvh, c0);
-    const uint16_t* vb = tile_base<D>(p, p.v, p.vp, kvh, c0);
-    if (kb != nullptr) {
-#pragma unroll
-      for (int j = 0; j < DMA_PER_WAVE; ++j) {
-        const int piece = wave * DMA_PER_WAVE + j;
-        const uint32_t kdst = lds_offset(&k_lds[st][piece * PIECE_ELEMS]);
-        const uint32_t vdst = lds_offset(&v_lds[st][piece * PIECE_ELEMS]);
-        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(koff[j]),
-                     "s"(kb), "s"(kdst)
-                     : "memory");
-        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff[j]),
-                     "s"(vb), "s"(vdst)
-                     : "memory");
-      }
-      return;
-    }
-#pragma unroll
-    for (int j = 0; j < DMA_PER_WAVE; ++j) {
-      const int piece = wave * DMA_PER_WAVE + j;
-      const int row = piece * ROWS_PER_PIECE + lane / KCH;
-      const int slot = lane % KCH;
-      const int c = min(c0 + row, p.Ktot - 1);
-      const uint16_t* ksrc = key_row<D>(p, p.k, p.kp, kvh, c) + 8 * (slot ^ k_swz<D>(row));
-      const uint16_t* vsrc = key_row<D>(p, p.v, p.vp, kvh, c) + 8 * (slot ^ v_swz<D>(row));
-      const uint32_t kdst = lds_offset(&k_lds[st][piece * PIECE_ELEMS]);
-      const uint32_t vdst = lds_offset(&v_lds[st][piece * PIECE_ELEMS]);
-      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(ksrc), "s"(kdst)
-                   : "memory");
-      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(vsrc), "s"(vdst)
-                   : "memory");
-    }
-  };
-  // Wait until this wave's copies of the tile issued before the most recent
-  // one have landed (`newer_issued`: whether a later tile's copies follow).
-  // `newer` = number of later tiles whose copies are already in flight.
-  auto dma_wait = [&](int newer) {
-    const int n = newer * 2 * DMA_PER_WAVE;
-    if (n >= 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else if (n >= 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
-    else if (n >= 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else if (n >= 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  };
-
-  // LDS operands.  QK step i (k over head_dim 16i .. 16i+15): A = K rows
-  // (lane n holds key n of the tile).  PV step i: 16-key group c = i / NDB,
-  // dim block db = i % NDB; pb[c] slot j of lane half hh holds key
-  // 16c + 8*(j/4) + 4*hh + j%4 (the S^T accumulator layout), and the A operand
-  // (dims x keys) comes from two transposing reads of 4 keys each: in a
-  // 16-lane group g, source lane sl addresses key row 16c + 8*rd + 4*(g/2) +
-  // sl/4 at dims 32*db + 16*(g%2) + 4*(sl%4) .. +3, and result lane i, slot j
-  // gets element i%4 of source lane 4j + i/4.
-  auto k_operand = [&](const uint16_t* kl, int i) -> bf16x8 {
-    return *reinterpret_cast<const bf16x8*>(&kl[n * D + 8 * ((2 * i + h) ^ k_swz<D>(n))]);
-  };
-  auto v_operand = [&](const uint16_t* vl, int i) -> bf16x8 {
-    const int c = i / NDB, db = i % NDB;
+  // LDS operands, addressed as (stage base + lane base) ^ (step bits) +
+  // immediate, so no per-step address registers stay live across tiles.
+  //  QK step i: k-step kc = i/2 over head_dim, key block i%2; the A operand
+  //  holds K rows (lane n holds key 32*(i%2) + n, chunk 2kc + h).  With the
+  //  K swizzle, chunk (2kc + h) of row n sits at byte 16*((h ^ n) & 1) +
+  //  16*(n & (KCH-2)) xor 32*kc of the row; the key block is the immediate.
+  //  PV step i: 16-key group c = i / NDB, dim block db = i % NDB; pb[c] slot
+  //  j of lane half hh holds key 16c + 8*(j/4) + 4*hh + j%4 (the S^T
+  //  accumulator layout), and the A operand (dims x keys) comes from two
+  //  transposing reads of 4 keys each: in a 16-lane group g, source lane sl
+  //  addresses key row 16c + 8*rd + 4*(g/2) + sl/4 at dims 32*db + 16*(g%2)
+  //  + 4*(sl%4) .. +3 (result lane i, slot j gets element i%4 of source
+  //  lane 4j + i/4).  With the V swizzle the dim block lands at byte
+  //  64*(db ^ (row & (NDB-1))) of the row, the rest of the lane's offset is
+  //  fixed, and (c, rd) is the immediate.
+  const uint32_t k_lane = (uint32_t)(n * 2 * D + 16 * ((h ^ n) & 1) + 16 * (n & (KCH - 2)));
+  uint32_t v_lane;
+  {
     const int g = lane >> 4, sl = lane & 15;
+    const int row = 4 * (g >> 1) + (sl >> 2);
+    v_lane = (uint32_t)(row * 2 * D + 64 * (row & (NDB - 1)) + 16 * (2 * (g & 1) + ((sl & 3) >> 1)) +
+                        8 * (sl & 1));
+  }
+  auto k_operand = [&](uint32_t kb, int i) -> bf16x8 {
+    const uint32_t a = (kb ^ (32u * (uint32_t)(i >> 1))) + (uint32_t)(64 * D * (i & 1));
+    return *(const lds_bf16x8*)(uintptr_t)a;
+  };
+  auto v_operand = [&](uint32_t vb, int i) -> bf16x8 {
+    const int c = i / NDB, db = i % NDB;
+    const uint32_t x = vb ^ (64u * (uint32_t)db);
     i16x4 part[2];
 #pragma unroll
-    for (int rd = 0; rd < 2; ++rd) {
-      const int row = 16 * c + 8 * rd + 4 * (g >> 1) + (sl >> 2);
-      const int dim = 32 * db + 16 * (g & 1) + 4 * (sl & 3);
-      const uint16_t* addr = &vl[row * D + 8 * ((dim >> 3) ^ v_swz<D>(row)) + (dim & 7)];
-      part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
-    }
+    for (int rd = 0; rd < 2; ++rd)
+      part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_i16x4*)(uintptr_t)(x + (uint32_t)((16 * c + 8 * rd) * 2 * D)));
     return __builtin_bit_cast(
         bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
   };
+  auto pv_step = [&](const bf16x8& a, int i) {
+    oacc[i % NDB] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[i / NDB], oacc[i % NDB], 0, 0, 0);
+  };
 
-  // Ring of kStages LDS stages: tile t lives in stage t % kStages; the copies
-  // of tile t+kAhead are issued at the start of tile t into the stage of
-  // tile t-1 (every wave has passed the barrier that ended tile t-1), and
-  // tile t+1 must have landed before the barrier that ends tile t.
+  // MFMA steps.  qk_pv(t) computes S(t) = K(t) Q^T and O += P(t-1) V(t-1),
+  // the two streams interleaved step by step with their LDS operands read PD
+  // steps ahead into rotating registers; qk_only and pv_only are the first
+  // and last tiles.  The scheduling barriers keep the prefetch distance (the
+  // compiler would otherwise hoist every read of the tile and run out of
+  // registers).
+  auto k_stage = [&](int t) { return lds_offset(k_lds[t % kStages]) + k_lane; };
+  auto v_stage = [&](int t) { return lds_offset(v_lds[t % kStages]) + v_lane; };
+  const f32x16 zero16 = {};
+  auto qk_pv = [&](int t) {
+    const uint32_t kl = k_stage(t), vl = v_stage(t - 1);
+    bf16x8 ka[PD + 1], va[PD + 1];
 #pragma unroll
-  for (int a = 0; a < kAhead; ++a)
-    if (a < ntiles) dma_tile(a, a);
-  dma_wait(min(ntiles, kAhead) - 1);
-  phase_barrier();
+    for (int i = 0; i < PD; ++i) {
+      ka[i] = k_operand(kl, i);
+      va[i] = v_operand(vl, i);
+    }
+#pragma unroll
+    for (int i = 0; i < NQK; ++i) {
+      if (i + PD < NQK) {
+        ka[(i + PD) % (PD + 1)] = k_operand(kl, i + PD);
+        va[(i + PD) % (PD + 1)] = v_operand(vl, i + PD);
+      }
+      s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % (PD + 1)], qreg[i >> 1],
+                                                         i < 2 ? zero16 : s[i & 1], 0, 0, 0);
+      pv_step(va[i % (PD + 1)], i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto qk_only = [&](int t) {
+    const uint32_t kl = k_stage(t);
+    bf16x8 ka[PD + 1];
+#pragma unroll
+    for (int i = 0; i < PD; ++i) ka[i] = k_operand(kl, i);
+#pragma unroll
+    for (int i = 0; i < NQK; ++i) {
+      if (i + PD < NQK) ka[(i + PD) % (PD + 1)] = k_operand(kl, i + PD);
+      s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % (PD + 1)], qreg[i >> 1],
+                                                         i < 2 ? zero16 : s[i & 1], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto pv_only = [&](int t) {
+    const uint32_t vl = v_stage(t);
+    bf16x8 va[PD + 1];
+#pragma unroll
+    for (int i = 0; i < PD; ++i) va[i] = v_operand(vl, i);
+#pragma unroll
+    for (int i = 0; i < NPV; ++i) {
+      if (i + PD < NPV) va[(i + PD) % (PD + 1)] = v_operand(vl, i + PD);
+      pv_step(va[i % (PD + 1)], i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
 
-  int st = 0;  // stage of tile t
-  for (int t = 0; t < ntiles; ++t) {
-    if (t + kAhead < ntiles) dma_tile(t + kAhead, st == 0 ? kStages - 1 : st - 1);
-    if (t < w_tiles) {
-      const uint16_t* kl = k_lds[st];
-      const uint16_t* vl = v_lds[st];
-      // S^T = K(t) Q^T per row block: lane (n, h) holds keys
-      // 8*(r/4) + 4*h + r%4 of query n.  Every K operand feeds kRB MFMAs.
-      f32x16 s[kRB];
+  // Softmax of tile t: mask, running max, exp2, row sums, P -> bf16.
+  auto softmax = [&](int t) {
+    const int c0 = t * kBN;
+    if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
 #pragma unroll
-      for (int b = 0; b < kRB; ++b)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[b][r] = 0.f;
-#pragma unroll
-      for (int i = 0; i < NKC; ++i) {
-        const bf16x8 a = k_operand(kl, i);
-#pragma unroll
-        for (int b = 0; b < kRB; ++b)
-          s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[b][i], s[b], 0, 0, 0);
-      }
-      const int c0 = t * kBN;
-      if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
-#pragma unroll
-        for (int b = 0; b < kRB; ++b)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (c >= rq_end[b]) s[b][r] = -INFINITY;
-          }
-      }
-      float m_blk[kRB];
-      bool grow = false;
-#pragma unroll
-      for (int b = 0; b < kRB; ++b) {
-        float mq[4];  // four independent max chains
-#pragma unroll
-        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[b][j], s[b][j + 4]);
-#pragma unroll
-        for (int r = 8; r < 16; r += 4)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[b][r + j]);
-        float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-        mx = fmaxf(mx, half_swap(mx));
-        m_blk[b] = mx * p.scale_log2;
-        grow = grow || (m_blk[b] > m_run[b] + kRescaleSlack);
-      }
-      // Lazy rescale: m_run only moves when some row's tile max exceeds it
-      // by more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack
-      // and O and l share the same (possibly stale) m_run; O / l and
-      // m_run*ln2 + ln(l) do not depend on the choice.
-      if (__any(grow)) {
-#pragma unroll
-        for (int b = 0; b < kRB; ++b) {
-          const float m_new = fmaxf(m_run[b], m_blk[b]);
-          const float alpha =
-              m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[b] - m_new);
-          m_run[b] = m_new;
-          l_run[b] *= alpha;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) oacc[b][db][r] *= alpha;
-        }
-      }
-      bf16x8 pb[kRB][2];
-#pragma unroll
-      for (int b = 0; b < kRB; ++b) {
-        float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
+      for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[b][r], p.scale_log2, -m_run[b]));
-          rs[r & 3] += e;
-          pb[b][r >> 3][r & 7] = (__bf16)e;
+          const int c = c0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (c >= rq_end) s[sb][r] = -INFINITY;
         }
-        l_run[b] += (rs[0] + rs[1]) + (rs[2] + rs[3]);
-      }
-#pragma unroll
-      for (int i = 0; i < 2 * NDB; ++i) {  // every V operand feeds kRB MFMAs
-        const bf16x8 a = v_operand(vl, i);
-#pragma unroll
-        for (int b = 0; b < kRB; ++b)
-          oacc[b][i % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[b][i / NDB],
-                                                                    oacc[b][i % NDB], 0, 0, 0);
-      }
     }
-    dma_wait(min(ntiles - 1 - (t + 1), kAhead - 1) < 0 ? 0 : min(ntiles - 1 - (t + 1), kAhead - 1));
+    float mq[4];  // four independent max chains
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j >> 1][8 * (j & 1)], s[j >> 1][8 * (j & 1) + 1]);
+#pragma unroll
+    for (int r = 2; r < 8; ++r)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j >> 1][8 * (j & 1) + r]);
+    float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+    mx = fmaxf(mx, half_swap(mx));
+    const float m_tile = mx * p.scale_log2;
+    // Lazy rescale: m_run only moves when some row's tile max exceeds it by
+    // more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack and
+    // O and l share the same (possibly stale) m_run; O / l and
+    // m_run*ln2 + ln(l) do not depend on the choice of m_run.
+    if (__any(m_tile > m_run + kRescaleSlack)) {
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    }
+    float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
+        rs[r & 3] += e;
+        pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
+      }
+    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+  };
+
+  // Tiles a wave's rows cannot see need no branch: the mask sets their
+  // logits to -inf, so their probabilities are 0 and the running max does
+  // not move.  The MFMA priority lets the MFMA wave win issue arbitration
+  // over the softmax wave sharing its SIMD.
+  auto mfma_prio = [] { __builtin_amdgcn_s_setprio(1); };
+  auto vmem_prio = [] { __builtin_amdgcn_s_setprio(0); };
+  if (grp == 0) {
+    // group A: copies V; MFMA(t) in phase 2t, softmax(t) in phase 2t+1
+    issue(0);
+    if (ntiles > 1) issue(1);
     phase_barrier();
-    st = st == kStages - 1 ? 0 : st + 1;
+    mfma_prio();
+    qk_only(0);
+    vmem_prio();
+    phase_barrier();
+    if (2 < ntiles) issue(2);
+    softmax(0);
+    land(min(ntiles - 1, 2));
+    phase_barrier();
+    for (int t = 1; t < ntiles; ++t) {
+      mfma_prio();
+      qk_pv(t);
+      vmem_prio();
+      phase_barrier();
+      if (t + 2 < ntiles) issue(t + 2);
+      softmax(t);
+      land(min(ntiles - 1 - t, 2));
+      phase_barrier();
+    }
+    mfma_prio();
+    pv_only(ntiles - 1);
+    vmem_prio();
+    phase_barrier();
+    phase_barrier();
+  } else {
+    // group B: copies K; MFMA(t) in phase 2t+1, softmax(t) in phase 2t+2
+    issue(0);
+    if (ntiles > 1) issue(1);
+    land(ntiles > 1 ? 1 : 0);
+    phase_barrier();
+    if (2 < ntiles) issue(2);
+    phase_barrier();
+    mfma_prio();
+    qk_only(0);
+    vmem_prio();
+    if (1 < ntiles) land(2 < ntiles ? 1 : 0);
+    phase_barrier();
+    if (3 < ntiles) issue(3);
+    softmax(0);
+    phase_barrier();
+    for (int t = 1; t < ntiles; ++t) {
+      mfma_prio();
+      qk_pv(t);
+      vmem_prio();
+      if (t + 1 < ntiles) land(t + 2 < ntiles ? 1 : 0);
+      phase_barrier();
+      if (t + 3 < ntiles) issue(t + 3);
+      softmax(t);
+      phase_barrier();
+    }
+    mfma_prio();
+    pv_only(ntiles - 1);
+    vmem_prio();
+    phase_barrier();
   }
 
-  if (!w_valid) return;
+  if (!w_valid || rq >= p.M) return;
+  const float l_tot = l_run + half_swap(l_run);
+  const float inv = 1.f / l_tot;
+  uint16_t* orow = p.o + ((size_t)head * p.M + rq) * D;
 #pragma unroll
-  for (int b = 0; b < kRB; ++b) {
-    const float l_tot = l_run[b] + half_swap(l_run[b]);
-    if (rq[b] >= p.M) continue;
-    const float inv = 1.f / l_tot;
-    uint16_t* orow = p.o + ((size_t)head * p.M + rq[b]) * D;
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 w;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        bf16x4 w;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) w[i] = (__bf16)(oacc[b][db][4 * g + i] * inv);
-        *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
-      }
-    if (p.lse && h == 0)
-      p.lse[(size_t)head * p.M + rq[b]] = m_run[b] * 0.69314718055994531f + logf(l_tot);
-  }
+      for (int i = 0; i < 4; ++i) w[i] = (__bf16)(oacc[db][4 * g + i] * inv);
+      *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
+    }
+  if (p.lse && h == 0) p.lse[(size_t)head * p.M + rq] = m_run * 0.69314718055994531f + logf(l_tot);
 }
 
 }  // namespace
