@@ -103,22 +103,9 @@ __device__ __forceinline__ void map_block(const Params& p, int bid, int& head, i
   }
 }
 
-// Address of concatenated key row c (0 <= c < Ktot) of KV head kvh.
-template <int D>
-__device__ __forceinline__ const uint16_t* key_row(const Params& p, const uint16_t* loc,
-                                                   const uint16_t* pass, int kvh, int c) {
-  if (c < p.La) return loc + ((size_t)kvh * p.M + c) * D;
-  if (c < p.La + p.Lp) {
-    const int t = c - p.La;
-    const int s = t / p.lp;
-    const int r = t - s * p.lp;
-    return pass + (((size_t)s * p.n_kv + kvh) * p.lp + r) * D;
-  }
-  return loc + ((size_t)kvh * p.M + (c - p.Lp)) * D;
-}
-
-// key_row without branches (per-lane selects), for copies whose rows may
-// fall into different segments.
+// Address of concatenated key row c (0 <= c < Ktot) of KV head kvh, with
+// per-lane selects instead of branches (the lanes of one copy may fall into
+// different segments).
 template <int D>
 __device__ __forceinline__ const uint16_t* key_row_sel(const Params& p, const uint16_t* loc,
                                                        const uint16_t* pass, int kvh, int c) {
@@ -129,24 +116,6 @@ __device__ __forceinline__ const uint16_t* key_row_sel(const Params& p, const ui
   const size_t pass_row = ((size_t)s * p.n_kv + kvh) * p.lp + r;
   const size_t loc_row = (size_t)kvh * p.M + (c < p.La ? c : c - p.Lp);
   return in_pass ? pass + pass_row * D : loc + loc_row * D;
-}
-
-// Base address of key tile [c0, c0 + kBN) when it lies inside one segment
-// (anchor, one passing slot, or the local block) and below Ktot; nullptr
-// when the tile straddles a boundary and rows must be looked up one by one.
-template <int D>
-__device__ __forceinline__ const uint16_t* tile_base(const Params& p, const uint16_t* loc,
-                                                     const uint16_t* pass, int kvh, int c0) {
-  if (c0 + kBN > p.Ktot) return nullptr;
-  if (c0 + kBN <= p.La) return loc + ((size_t)kvh * p.M + c0) * D;
-  if (c0 >= p.La + p.Lp) return loc + ((size_t)kvh * p.M + (c0 - p.Lp)) * D;
-  if (c0 >= p.La && c0 + kBN <= p.La + p.Lp) {
-    const int t = c0 - p.La;
-    const int s = t / p.lp;
-    const int r = t - s * p.lp;
-    if (r + kBN <= p.lp) return pass + (((size_t)s * p.n_kv + kvh) * p.lp + r) * D;
-  }
-  return nullptr;
 }
 
 // Value held by the lane 32 apart (the other half of the wave holds the
@@ -168,6 +137,14 @@ template <int D>
 __device__ __forceinline__ int k_swz(int r) { return r & (D / 8 - 1); }
 template <int D>
 __device__ __forceinline__ int v_swz(int r) { return (4 * (r & 3)) & (D / 8 - 1); }
+
+// A wave-uniform 64-bit value in scalar registers (the copies take their
+// base address and M0 from SGPRs).
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
 
 // Byte offset of an LDS location, as M0 and LDS instructions address it.
 __device__ __forceinline__ uint32_t lds_offset(const uint16_t* p) {
@@ -228,33 +205,73 @@ attn_fwd_kernel(Params p) {
   // T % kStages, whose previous tile was last read in phase 2T-5; each waits
   // for its copy just before the barrier that opens the consuming phase.
 
-  // Copy lanes: global_load_lds_dwordx4 puts lane l's 16 bytes at M0 + 16*l,
-  // so each instruction fills one 1 KiB piece of the swizzled tile and every
-  // lane fetches the chunk that belongs at its slot.  The copies are inline
-  // asm so the compiler does not order the LDS operand reads behind them.
+  // Copy lanes: global_load_lds_dwordx4 puts lane l's 16 bytes at M0 +
+  // inst_offset + 16*l and reads them from saddr + voffset + inst_offset, so
+  // one M0 serves the wave's WP pieces (1 KiB apart in LDS and, inside one
+  // segment, in HBM) and every lane fetches the chunk that belongs at its
+  // swizzled slot.  The copies are inline asm so the compiler does not order
+  // the LDS operand reads behind them.
   const bool copies_v = grp == 0;
   const uint16_t* cp_loc = copies_v ? p.v : p.k;
   const uint16_t* cp_pass = copies_v ? p.vp : p.kp;
-  uint32_t cp_off[WP];
+  uint32_t cp_off[WP];  // per-lane byte offset of piece j, less j KiB
 #pragma unroll
   for (int j = 0; j < WP; ++j) {
     const int row = (wig * WP + j) * ROWS_PER_PIECE + lane / KCH;
     const int slot = lane % KCH;
     const int swz = copies_v ? v_swz<D>(row) : k_swz<D>(row);
-    cp_off[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ swz));
+    cp_off[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ swz)) - 1024u * j;
   }
-  auto issue = [&](int T) {
+  // Segment cursor: concatenated key rows c in [.., seg_end) sit at byte
+  // address seg_base + 2*D*c.  Tiles are copied in increasing order, so the
+  // cursor moves only when a tile starts at or past seg_end.
+  uint64_t seg_base = 0;
+  int seg_end = 0;
+  auto seek = [&](int c0) __attribute__((always_inline)) {
+    if (c0 < p.La) {
+      seg_end = p.La;
+      seg_base = (uint64_t)cp_loc + (uint64_t)(2 * D) * ((uint64_t)kvh * p.M);
+    } else if (c0 < p.La + p.Lp) {
+      const int sl = (c0 - p.La) / p.lp;
+      seg_end = p.La + (sl + 1) * p.lp;
+      seg_base = (uint64_t)cp_pass +
+                 (uint64_t)(2 * D) * (uint64_t)((int64_t)(sl * p.n_kv + kvh) * p.lp -
+                                                (p.La + (int64_t)sl * p.lp));
+    } else {
+      seg_end = p.Ktot;
+      seg_base = (uint64_t)cp_loc + (uint64_t)(2 * D) * (uint64_t)((int64_t)kvh * p.M - p.Lp);
+    }
+  };
+  auto issue = [&](int T) __attribute__((always_inline)) {
     const int c0 = T * kBN;
-    const uint16_t* base = tile_base<D>(p, cp_loc, cp_pass, kvh, c0);
+    if (c0 >= seg_end) seek(c0);
     uint16_t* stage = copies_v ? v_lds[T % kStages] : k_lds[T % kStages];
-#pragma unroll
-    for (int j = 0; j < WP; ++j) {
-      const uint32_t dst = lds_offset(&stage[(wig * WP + j) * PIECE_ELEMS]);
-      if (base != nullptr) {
-        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(cp_off[j]),
-                     "s"(base), "s"(dst)
-                     : "memory", "m0");
+    if (c0 + kBN <= seg_end) {
+      const uint64_t base = uniform64(seg_base + (uint64_t)(2 * D) * (uint32_t)c0);
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_offset(&stage[wig * WP * PIECE_ELEMS]));
+      if constexpr (WP == 4) {
+        asm volatile(
+            "s_mov_b32 m0, %5\n\t"
+            "global_load_lds_dwordx4 %0, %4\n\t"
+            "global_load_lds_dwordx4 %1, %4 offset:1024\n\t"
+            "global_load_lds_dwordx4 %2, %4 offset:2048\n\t"
+            "global_load_lds_dwordx4 %3, %4 offset:3072" ::"v"(cp_off[0]),
+            "v"(cp_off[1]), "v"(cp_off[2]), "v"(cp_off[3]), "s"(base), "s"(dst)
+            : "memory", "m0");
       } else {
+        asm volatile(
+            "s_mov_b32 m0, %3\n\t"
+            "global_load_lds_dwordx4 %0, %2\n\t"
+            "global_load_lds_dwordx4 %1, %2 offset:1024" ::"v"(cp_off[0]),
+            "v"(cp_off[1]), "s"(base), "s"(dst)
+            : "memory", "m0");
+      }
+    } else {
+      // tile straddles a segment end (or the end of the keys): rows are
+      // looked up one by one, rows past the end repeat the last key
+#pragma unroll
+      for (int j = 0; j < WP; ++j) {
+        const uint32_t dst = lds_offset(&stage[(wig * WP + j) * PIECE_ELEMS]);
         const int row = (wig * WP + j) * ROWS_PER_PIECE + lane / KCH;
         const int slot = lane % KCH;
         const int c = min(c0 + row, p.Ktot - 1);
@@ -267,7 +284,7 @@ attn_fwd_kernel(Params p) {
   };
   // Wait until this wave's copies of tile T have landed, `later` of its
   // copies of later tiles being allowed to stay in flight.
-  auto land = [&](int later) {
+  auto land = [&](int later) __attribute__((always_inline)) {
     if (later >= 2) {
       if constexpr (WP == 4) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
       else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
@@ -330,11 +347,11 @@ attn_fwd_kernel(Params p) {
     v_lane = (uint32_t)(row * 2 * D + 64 * (row & (NDB - 1)) + 16 * (2 * (g & 1) + ((sl & 3) >> 1)) +
                         8 * (sl & 1));
   }
-  auto k_operand = [&](uint32_t kb, int i) -> bf16x8 {
+  auto k_operand = [&](uint32_t kb, int i) -> bf16x8 __attribute__((always_inline)) {
     const uint32_t a = (kb ^ (32u * (uint32_t)(i >> 1))) + (uint32_t)(64 * D * (i & 1));
     return *(const lds_bf16x8*)(uintptr_t)a;
   };
-  auto v_operand = [&](uint32_t vb, int i) -> bf16x8 {
+  auto v_operand = [&](uint32_t vb, int i) -> bf16x8 __attribute__((always_inline)) {
     const int c = i / NDB, db = i % NDB;
     const uint32_t x = vb ^ (64u * (uint32_t)db);
     i16x4 part[2];
@@ -345,7 +362,7 @@ attn_fwd_kernel(Params p) {
     return __builtin_bit_cast(
         bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  auto pv_step = [&](const bf16x8& a, int i) {
+  auto pv_step = [&](const bf16x8& a, int i) __attribute__((always_inline)) {
     oacc[i % NDB] =
         __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[i / NDB], oacc[i % NDB], 0, 0, 0);
   };
@@ -353,19 +370,32 @@ attn_fwd_kernel(Params p) {
   // MFMA steps.  qk_pv(t) computes S(t) = K(t) Q^T and O += P(t-1) V(t-1),
   // the two streams interleaved step by step with their LDS operands read PD
   // steps ahead into rotating registers; qk_only and pv_only are the first
-  // and last tiles.  The scheduling barriers keep the prefetch distance (the
-  // compiler would otherwise hoist every read of the tile and run out of
-  // registers).
-  auto k_stage = [&](int t) { return lds_offset(k_lds[t % kStages]) + k_lane; };
-  auto v_stage = [&](int t) { return lds_offset(v_lds[t % kStages]) + v_lane; };
+  // and last tiles.  The first PD steps' operands (kpre, vpre) are read at
+  // the end of the wave's preceding softmax phase, so an MFMA phase starts
+  // with its operands in registers.  The scheduling barriers keep the
+  // prefetch distance (the compiler would otherwise hoist every read of the
+  // tile and run out of registers).
+  auto k_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(k_lds[t % kStages]) + k_lane; };
+  auto v_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(v_lds[t % kStages]) + v_lane; };
   const f32x16 zero16 = {};
-  auto qk_pv = [&](int t) {
+  bf16x8 kpre[PD], vpre[PD];
+  auto pre_k = [&](int t) __attribute__((always_inline)) {
+    const uint32_t kl = k_stage(t);
+#pragma unroll
+    for (int i = 0; i < PD; ++i) kpre[i] = k_operand(kl, i);
+  };
+  auto pre_v = [&](int t) __attribute__((always_inline)) {
+    const uint32_t vl = v_stage(t);
+#pragma unroll
+    for (int i = 0; i < PD; ++i) vpre[i] = v_operand(vl, i);
+  };
+  auto qk_pv = [&](int t) __attribute__((always_inline)) {
     const uint32_t kl = k_stage(t), vl = v_stage(t - 1);
     bf16x8 ka[PD + 1], va[PD + 1];
 #pragma unroll
     for (int i = 0; i < PD; ++i) {
-      ka[i] = k_operand(kl, i);
-      va[i] = v_operand(vl, i);
+      ka[i] = kpre[i];
+      va[i] = vpre[i];
     }
 #pragma unroll
     for (int i = 0; i < NQK; ++i) {
@@ -379,11 +409,11 @@ attn_fwd_kernel(Params p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto qk_only = [&](int t) {
+  auto qk_only = [&](int t) __attribute__((always_inline)) {
     const uint32_t kl = k_stage(t);
     bf16x8 ka[PD + 1];
 #pragma unroll
-    for (int i = 0; i < PD; ++i) ka[i] = k_operand(kl, i);
+    for (int i = 0; i < PD; ++i) ka[i] = kpre[i];
 #pragma unroll
     for (int i = 0; i < NQK; ++i) {
       if (i + PD < NQK) ka[(i + PD) % (PD + 1)] = k_operand(kl, i + PD);
@@ -392,11 +422,11 @@ attn_fwd_kernel(Params p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto pv_only = [&](int t) {
+  auto pv_only = [&](int t) __attribute__((always_inline)) {
     const uint32_t vl = v_stage(t);
     bf16x8 va[PD + 1];
 #pragma unroll
-    for (int i = 0; i < PD; ++i) va[i] = v_operand(vl, i);
+    for (int i = 0; i < PD; ++i) va[i] = vpre[i];
 #pragma unroll
     for (int i = 0; i < NPV; ++i) {
       if (i + PD < NPV) va[(i + PD) % (PD + 1)] = v_operand(vl, i + PD);
@@ -404,9 +434,14 @@ attn_fwd_kernel(Params p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  // operands of the MFMA phase that follows softmax(t)
+  auto prefetch_after = [&](int t) __attribute__((always_inline)) {
+    if (t + 1 < ntiles) pre_k(t + 1);
+    pre_v(t);
+  };
 
   // Softmax of tile t: mask, running max, exp2, row sums, P -> bf16.
-  auto softmax = [&](int t) {
+  auto softmax = [&](int t) __attribute__((always_inline)) {
     const int c0 = t * kBN;
     if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
 #pragma unroll
@@ -457,30 +492,39 @@ attn_fwd_kernel(Params p) {
   // logits to -inf, so their probabilities are 0 and the running max does
   // not move.  The MFMA priority lets the MFMA wave win issue arbitration
   // over the softmax wave sharing its SIMD.
-  auto mfma_prio = [] { __builtin_amdgcn_s_setprio(1); };
-  auto vmem_prio = [] { __builtin_amdgcn_s_setprio(0); };
+  auto mfma_prio = []() __attribute__((always_inline)) { __builtin_amdgcn_s_setprio(1); };
+  auto vmem_prio = []() __attribute__((always_inline)) { __builtin_amdgcn_s_setprio(0); };
+  // Copy schedule: group B copies K(T) in phase 2T-4 and waits for it at the
+  // end of phase 2T-2; group A copies V(T) in phase 2T-3 and waits for it at
+  // the end of phase 2T-1.  The barrier after each wait makes the tile
+  // visible to the prefetch at the end of the phase before its first MFMA
+  // phase.  Ring stage T % 4 is rewritten only after its previous tile's last
+  // reader (phase 2T-7 for K, 2T-5 for V).
   if (grp == 0) {
     // group A: copies V; MFMA(t) in phase 2t, softmax(t) in phase 2t+1
     issue(0);
     if (ntiles > 1) issue(1);
+    land(ntiles > 1 ? 1 : 0);  // V(0)
     phase_barrier();
+    pre_k(0);
     mfma_prio();
     qk_only(0);
     vmem_prio();
     phase_barrier();
-    if (2 < ntiles) issue(2);
-    softmax(0);
-    land(min(ntiles - 1, 2));
-    phase_barrier();
+    auto a_softmax_phase = [&](int t) __attribute__((always_inline)) {
+      if (t + 2 < ntiles) issue(t + 2);
+      softmax(t);
+      prefetch_after(t);
+      if (t + 1 < ntiles) land(t + 2 < ntiles ? 1 : 0);  // V(t+1)
+      phase_barrier();
+    };
+    a_softmax_phase(0);
     for (int t = 1; t < ntiles; ++t) {
       mfma_prio();
       qk_pv(t);
       vmem_prio();
       phase_barrier();
-      if (t + 2 < ntiles) issue(t + 2);
-      softmax(t);
-      land(min(ntiles - 1 - t, 2));
-      phase_barrier();
+      a_softmax_phase(t);
     }
     mfma_prio();
     pv_only(ntiles - 1);
@@ -491,27 +535,30 @@ attn_fwd_kernel(Params p) {
     // group B: copies K; MFMA(t) in phase 2t+1, softmax(t) in phase 2t+2
     issue(0);
     if (ntiles > 1) issue(1);
-    land(ntiles > 1 ? 1 : 0);
+    land(ntiles > 1 ? 1 : 0);  // K(0)
     phase_barrier();
     if (2 < ntiles) issue(2);
+    pre_k(0);
+    if (1 < ntiles) land(2 < ntiles ? 1 : 0);  // K(1)
     phase_barrier();
+    auto b_softmax_phase = [&](int t) __attribute__((always_inline)) {
+      if (t + 3 < ntiles) issue(t + 3);
+      softmax(t);
+      prefetch_after(t);
+      if (t + 2 < ntiles) land(t + 3 < ntiles ? 1 : 0);  // K(t+2)
+      phase_barrier();
+    };
     mfma_prio();
     qk_only(0);
     vmem_prio();
-    if (1 < ntiles) land(2 < ntiles ? 1 : 0);
     phase_barrier();
-    if (3 < ntiles) issue(3);
-    softmax(0);
-    phase_barrier();
+    b_softmax_phase(0);
     for (int t = 1; t < ntiles; ++t) {
       mfma_prio();
       qk_pv(t);
       vmem_prio();
-      if (t + 1 < ntiles) land(t + 2 < ntiles ? 1 : 0);
       phase_barrier();
-      if (t + 3 < ntiles) issue(t + 3);
-      softmax(t);
-      phase_barrier();
+      b_softmax_phase(t);
     }
     mfma_prio();
     pv_only(ntiles - 1);
