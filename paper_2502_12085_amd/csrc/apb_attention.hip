@@ -33,8 +33,9 @@
 //    is one XOR of a per-lane base plus an immediate.
 //  * Online softmax in fp32 registers in base 2 (scale*log2(e) folded into one
 //    FMA), probabilities rounded to bf16 for the PV product, fp32 accumulate.
-//    The running max moves lazily (only when it grows by more than 2^8), so
-//    the O rescale is off the common path.
+//    The running max moves lazily: probabilities are formed against the
+//    current max and the tile max is only computed when a tile's row sum
+//    exceeds 2^13, so the max pass and the O rescale are off the common path.
 //  * Tiles crossing a row's visible end are masked element-wise; tiles past
 //    every row of the workgroup are not visited.
 //  * Grid order puts the query tiles with the longest key prefix first, and
@@ -65,7 +66,7 @@ constexpr int kStages = 4;                         // LDS ring depth for K and V
 #define APB_PD 2
 #endif
 constexpr int kXcds = 8;                    // MI355X: 8 XCDs, workgroups dealt round-robin
-constexpr float kRescaleSlack = 8.f;        // lazy rescale threshold, base-2 units
+constexpr float kSumLimit = 8192.f;         // lazy rescale: largest tile row-half sum against a stale max
 
 struct Params {
   const uint16_t* q;
@@ -452,22 +453,40 @@ attn_fwd_kernel(Params p) {
           if (c >= rq_end) s[sb][r] = -INFINITY;
         }
     }
-    float mq[4];  // four independent max chains
+    // Lazy running max without a max pass on the common path: the
+    // probabilities are taken against the current (possibly stale) m_run,
+    // and only when some row-half's tile sum exceeds kSumLimit (a logit far
+    // above m_run, or the first tile, where m_run = -inf) does the wave find
+    // the tile max,
+    // move m_run up to it, rescale O and l, and redo the tile.  O and l
+    // share one m_run per row, and O / l and m_run*ln2 + ln(l) do not depend
+    // on its value.
+    float rs[4];
+    auto exp_tile = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j >> 1][8 * (j & 1)], s[j >> 1][8 * (j & 1) + 1]);
+      for (int j = 0; j < 4; ++j) rs[j] = 0.f;  // four independent sum chains
 #pragma unroll
-    for (int r = 2; r < 8; ++r)
+      for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j >> 1][8 * (j & 1) + r]);
-    float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-    mx = fmaxf(mx, half_swap(mx));
-    const float m_tile = mx * p.scale_log2;
-    // Lazy rescale: m_run only moves when some row's tile max exceeds it by
-    // more than 2^kRescaleSlack, so exp2 arguments stay <= kRescaleSlack and
-    // O and l share the same (possibly stale) m_run; O / l and
-    // m_run*ln2 + ln(l) do not depend on the choice of m_run.
-    if (__any(m_tile > m_run + kRescaleSlack)) {
-      const float m_new = fmaxf(m_run, m_tile);
+        for (int r = 0; r < 16; ++r) {
+          const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
+          rs[r & 3] += e;
+          pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
+        }
+    };
+    exp_tile();
+    const float l_tile = (rs[0] + rs[1]) + (rs[2] + rs[3]);
+    if (__any(!(l_tile <= kSumLimit))) {
+      float mq[4];  // four independent max chains
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j >> 1][8 * (j & 1)], s[j >> 1][8 * (j & 1) + 1]);
+#pragma unroll
+      for (int r = 2; r < 8; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j >> 1][8 * (j & 1) + r]);
+      float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+      mx = fmaxf(mx, half_swap(mx));
+      const float m_new = fmaxf(m_run, mx * p.scale_log2);
       const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
       l_run *= alpha;
@@ -475,16 +494,8 @@ attn_fwd_kernel(Params p) {
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      exp_tile();
     }
-    float rs[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sum chains
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
-        rs[r & 3] += e;
-        pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
-      }
     l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
   };
 
