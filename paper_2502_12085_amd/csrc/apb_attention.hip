@@ -461,21 +461,36 @@ attn_fwd_kernel(Params p) {
     // move m_run up to it, rescale O and l, and redo the tile.  O and l
     // share one m_run per row, and O / l and m_run*ln2 + ln(l) do not depend
     // on its value.
-    float rs[4];
+    // The tile is processed in three batches (all FMAs, all exp2, then the
+    // sums and bf16 packing) so that no instruction waits on the latency of
+    // the one before it: a lone wave issues VALU work slowly enough already.
+    float rs[8];
     auto exp_tile = [&]() __attribute__((always_inline)) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) rs[j] = 0.f;  // four independent sum chains
+      f32x16 e[2];
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
-          rs[r & 3] += e;
-          pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e;
-        }
+        for (int r = 0; r < 16; ++r) e[sb][r] = fmaf(s[sb][r], p.scale_log2, -m_run);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) e[sb][r] = __builtin_amdgcn_exp2f(e[sb][r]);
+      __builtin_amdgcn_sched_barrier(0);
+      // eight independent sum chains, chain j over elements 4j .. 4j+3
+#pragma unroll
+      for (int j = 0; j < 8; ++j) rs[j] = e[j >> 2][4 * (j & 3)];
+#pragma unroll
+      for (int k = 1; k < 4; ++k)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) rs[j] += e[j >> 2][4 * (j & 3) + k];
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e[sb][r];
     };
     exp_tile();
-    const float l_tile = (rs[0] + rs[1]) + (rs[2] + rs[3]);
+    const float l_tile = ((rs[0] + rs[1]) + (rs[2] + rs[3])) + ((rs[4] + rs[5]) + (rs[6] + rs[7]));
     if (__any(!(l_tile <= kSumLimit))) {
       float mq[4];  // four independent max chains
 #pragma unroll
@@ -496,7 +511,7 @@ attn_fwd_kernel(Params p) {
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
       exp_tile();
     }
-    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+    l_run += ((rs[0] + rs[1]) + (rs[2] + rs[3])) + ((rs[4] + rs[5]) + (rs[6] + rs[7]));
   };
 
   // Tiles a wave's rows cannot see need no branch: the mask sets their
