@@ -15,3 +15,9 @@ from .apb_oracle import (  # noqa: F401
     simulate_hosts_ref,
     attention_flops,
 )
+from .decode_oracle import (  # noqa: F401
+    decode_attention_ref,
+    merge_ref,
+    stage2_ref,
+    decode_bytes,
+)
