@@ -15,7 +15,11 @@
  *                        the selected K/V rows (Sec. 3.4; Alg. 2, compression
  *                        step);
  *   apb_attention_fwd    the modified-mask attention (Eq. 2; Alg. 2,
- *                        attention step).
+ *                        attention step);
+ * and the decoding stage that follows the prefill (Alg. 3):
+ *   apb_decode_attention one host's exact attention of the new tokens over
+ *                        its KV cache, with the LSE;
+ *   apb_merge_partials   MergeScore of the hosts' partial results.
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are caller-owned DEVICE memory on the current HIP
@@ -40,7 +44,7 @@
 extern "C" {
 #endif
 
-#define APB_ABI_VERSION 1
+#define APB_ABI_VERSION 2
 
 typedef enum {
   APB_OK = 0,
@@ -119,6 +123,74 @@ apb_status_t apb_attention_fwd(const apb_problem_t* p, const uint16_t* q,
                                const uint16_t* k_pass, const uint16_t* v_pass,
                                uint16_t* o, float* lse, float softmax_scale,
                                void* stream);
+
+/* ------------------------------------------------------------------------
+ * Decoding stage (stage 2, Alg. 3).  Every host attends the new tokens'
+ * queries to its own KV cache (its local block; Alg. 1 keeps K_h, V_h), the
+ * last host after appending the new tokens' own K/V; the hosts' partial
+ * outputs are then gathered and merged by their LSE (MergeScore).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_q_heads;  /* n_q >= 1, a multiple of n_kv                        */
+  int32_t n_kv_heads; /* n_kv >= 1; query head i reads KV head i / (n_q/n_kv) */
+  int32_t head_dim;   /* d, in {64, 128}                                     */
+  int32_t cache_len;  /* Lc >= 0 rows in this host's KV cache                */
+  int32_t n_new;      /* >= 1 new tokens (the question tokens at the first
+                         decoding step, one generated token afterwards)     */
+  int32_t append_new; /* 1 on the last host: the new tokens' K/V follow the
+                         cache and new token j sees new tokens 0..j (causal);
+                         0: the cache only                                   */
+} apb_decode_problem_t;
+
+/* Host-only checks of a decode problem (no HIP call). */
+apb_status_t apb_validate_decode(const apb_decode_problem_t* p);
+
+/* Bytes of device workspace apb_decode_attention needs for `p` (host only;
+ * depends on the shapes only). */
+apb_status_t apb_decode_workspace_size(const apb_decode_problem_t* p, uint64_t* bytes);
+
+/*
+ * apb_decode_attention -- one host's partial attention of a decoding step
+ * (Alg. 3, the attention lines), exact softmax over the visible keys.
+ *
+ *   q        bf16 [n_q][n_new][d]   the new tokens' queries.
+ *   k_cache, v_cache bf16 [n_kv][Lc][d]  this host's cache; ignored (may be
+ *                                   NULL) when Lc == 0.
+ *   k_new, v_new bf16 [n_kv][n_new][d]  the new tokens' keys/values; required
+ *                                   when append_new, ignored otherwise.
+ *   o_part   fp32 [n_q][n_new][d]   this host's partial output A_h.
+ *   lse_part fp32 [n_q][n_new]      its natural-log LSE (what Gather and
+ *                                   MergeScore need); a row with no visible
+ *                                   key gets o = 0, lse = -inf.
+ *   softmax_scale  as in apb_attention_fwd.
+ *   workspace, workspace_bytes  caller-owned device scratch of at least
+ *                   apb_decode_workspace_size() bytes, 16-byte aligned; the
+ *                   call overwrites it (calls that overlap in time must not
+ *                   share one).  The library allocates nothing.
+ * Arithmetic: bf16 inputs, fp32 dot products and softmax, probabilities
+ * rounded to bf16 for the value product, fp32 accumulation and output.
+ */
+apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t* q,
+                                  const uint16_t* k_cache, const uint16_t* v_cache,
+                                  const uint16_t* k_new, const uint16_t* v_new,
+                                  float* o_part, float* lse_part, float softmax_scale,
+                                  void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * apb_merge_partials -- MergeScore of Alg. 3: given P partial results
+ * (A_p, lse_p) of the same rows over disjoint key sets, the result over all
+ * the keys: lse = ln sum_p exp(lse_p), A = sum_p exp(lse_p - lse) A_p.
+ *
+ *   o_parts   fp32 [n_parts][rows][d]   (e.g. the gathered o_part of H hosts)
+ *   lse_parts fp32 [n_parts][rows]
+ *   o         bf16 [rows][d]            rounded to nearest even.
+ *   lse       fp32 [rows]               may be NULL.
+ * n_parts >= 1, rows >= 0, d in {64, 128}.  A part with lse = -inf adds
+ * nothing; a row whose parts are all -inf gets o = 0, lse = -inf.
+ */
+apb_status_t apb_merge_partials(int32_t n_parts, int32_t rows, int32_t head_dim,
+                                const float* o_parts, const float* lse_parts, uint16_t* o,
+                                float* lse, void* stream);
 
 /* Host-only checks of a problem description (no HIP call). */
 apb_status_t apb_validate_problem(const apb_problem_t* p);

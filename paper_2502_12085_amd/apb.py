@@ -18,7 +18,9 @@ STATUS_NAMES = {0: "APB_OK", 1: "APB_ERR_NULL_POINTER", 2: "APB_ERR_BAD_SHAPE",
                 3: "APB_ERR_UNSUPPORTED", 4: "APB_ERR_MISALIGNED", 5: "APB_ERR_HIP",
                 6: "APB_ERR_ALIAS"}
 EXPORTED = ("apb_compress_select", "apb_attention_fwd", "apb_validate_problem",
-            "apb_attention_flops", "apb_status_string", "apb_last_error", "apb_abi_version")
+            "apb_attention_flops", "apb_status_string", "apb_last_error", "apb_abi_version",
+            "apb_validate_decode", "apb_decode_workspace_size", "apb_decode_attention",
+            "apb_merge_partials")
 
 
 class ApbError(RuntimeError):
@@ -41,6 +43,20 @@ class Problem(ctypes.Structure):
     @classmethod
     def of(cls, p) -> "Problem":
         """From any object with the same field names (e.g. inputs.Problem)."""
+        return cls(*(int(getattr(p, f)) for f, _ in cls._fields_))
+
+
+class DecodeProblem(ctypes.Structure):
+    """``apb_decode_problem_t``: one host's decoding step (Alg. 3)."""
+
+    _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("cache_len", ctypes.c_int32),
+                ("n_new", ctypes.c_int32), ("append_new", ctypes.c_int32)]
+
+    @classmethod
+    def of(cls, p) -> "DecodeProblem":
+        if isinstance(p, cls):
+            return p
         return cls(*(int(getattr(p, f)) for f, _ in cls._fields_))
 
 
@@ -70,6 +86,17 @@ def lib() -> ctypes.CDLL:
         L.apb_last_error.restype = ctypes.c_char_p
         L.apb_abi_version.argtypes = []
         L.apb_abi_version.restype = ctypes.c_int
+        dp = ctypes.POINTER(DecodeProblem)
+        L.apb_validate_decode.argtypes = [dp]
+        L.apb_validate_decode.restype = ctypes.c_int
+        L.apb_decode_workspace_size.argtypes = [dp, ctypes.POINTER(ctypes.c_uint64)]
+        L.apb_decode_workspace_size.restype = ctypes.c_int
+        L.apb_decode_attention.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp,
+                                           ctypes.c_uint64, vp]
+        L.apb_decode_attention.restype = ctypes.c_int
+        L.apb_merge_partials.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp, vp,
+                                         vp, vp, vp]
+        L.apb_merge_partials.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -143,3 +170,46 @@ def attention_flops(problem) -> float:
 
 def abi_version() -> int:
     return lib().apb_abi_version()
+
+
+def validate_decode(problem) -> int:
+    return lib().apb_validate_decode(ctypes.byref(DecodeProblem.of(problem)))
+
+
+def decode_workspace_size(problem) -> int:
+    """``apb_decode_workspace_size``: device scratch bytes a decode call needs."""
+    n = ctypes.c_uint64(0)
+    _check(lib().apb_decode_workspace_size(ctypes.byref(DecodeProblem.of(problem)),
+                                           ctypes.byref(n)), "apb_decode_workspace_size")
+    return int(n.value)
+
+
+def decode_attention(problem, q, k_cache, v_cache, k_new, v_new, o_part, lse_part, workspace,
+                     softmax_scale=0.0, stream=None):
+    """``apb_decode_attention``: one host's stage-2 partial attention (Alg. 3).
+    ``workspace`` is a device tensor of at least ``decode_workspace_size``
+    bytes (any dtype)."""
+    import torch
+    b = _bf16_types()
+    f = (torch.float32,)
+    if workspace is None or not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous device tensor")
+    st = lib().apb_decode_attention(
+        ctypes.byref(DecodeProblem.of(problem)), _ptr(q, "q", b), _ptr(k_cache, "k_cache", b),
+        _ptr(v_cache, "v_cache", b), _ptr(k_new, "k_new", b), _ptr(v_new, "v_new", b),
+        _ptr(o_part, "o_part", f), _ptr(lse_part, "lse_part", f), float(softmax_scale),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "apb_decode_attention")
+
+
+def merge_partials(o_parts, lse_parts, o, lse=None, stream=None):
+    """``apb_merge_partials``: MergeScore (Alg. 3) of ``o_parts`` [P, rows, d]
+    (fp32) with ``lse_parts`` [P, rows] into ``o`` [rows, d] (bf16)."""
+    import torch
+    f = (torch.float32,)
+    n_parts, rows, d = o_parts.shape
+    st = lib().apb_merge_partials(
+        int(n_parts), int(rows), int(d), _ptr(o_parts, "o_parts", f),
+        _ptr(lse_parts, "lse_parts", f), _ptr(o, "o", _bf16_types()), _ptr(lse, "lse", f),
+        _stream(stream))
+    _check(st, "apb_merge_partials")

@@ -164,4 +164,114 @@ apb_status_t apb_attention_fwd(const apb_problem_t* p, const uint16_t* q, const 
   return APB_OK;
 }
 
+apb_status_t apb_validate_decode(const apb_decode_problem_t* p) {
+  if (!p) return APB_ERR_NULL_POINTER;
+  if (p->n_kv_heads < 1 || p->n_q_heads < 1 || p->n_q_heads % p->n_kv_heads != 0)
+    return APB_ERR_BAD_SHAPE;
+  if (p->cache_len < 0 || p->n_new < 1 || (p->append_new != 0 && p->append_new != 1))
+    return APB_ERR_BAD_SHAPE;
+  if (p->head_dim < 1) return APB_ERR_BAD_SHAPE;
+  if ((int64_t)p->cache_len + p->n_new > kMaxRows) return APB_ERR_BAD_SHAPE;
+  // rows of one GQA group and of the whole call stay well inside int32
+  if ((int64_t)p->n_q_heads * p->n_new > kMaxRows) return APB_ERR_BAD_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 128) return APB_ERR_UNSUPPORTED;
+  return APB_OK;
+}
+
+static apb::DecodeArgs decode_args(const apb_decode_problem_t* p) {
+  apb::DecodeArgs a{};
+  a.Lc = p->cache_len; a.n_new = p->n_new; a.append = p->append_new;
+  a.n_q = p->n_q_heads; a.n_kv = p->n_kv_heads; a.head_dim = p->head_dim;
+  return a;
+}
+
+apb_status_t apb_decode_workspace_size(const apb_decode_problem_t* p, uint64_t* bytes) {
+  const apb_status_t st = apb_validate_decode(p);
+  if (st != APB_OK) return st;
+  if (!bytes) return APB_ERR_NULL_POINTER;
+  *bytes = apb::plan_decode(decode_args(p)).workspace_bytes;
+  return APB_OK;
+}
+
+apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t* q,
+                                  const uint16_t* k_cache, const uint16_t* v_cache,
+                                  const uint16_t* k_new, const uint16_t* v_new, float* o_part,
+                                  float* lse_part, float softmax_scale, void* workspace,
+                                  uint64_t workspace_bytes, void* stream) {
+  const apb_status_t st = apb_validate_decode(p);
+  if (st != APB_OK) return st;
+  const bool has_cache = p->cache_len > 0, app = p->append_new == 1;
+  if (!q || !o_part || !lse_part || !workspace) return APB_ERR_NULL_POINTER;
+  if (has_cache && (!k_cache || !v_cache)) return APB_ERR_NULL_POINTER;
+  if (app && (!k_new || !v_new)) return APB_ERR_NULL_POINTER;
+  if (!aligned(q, 16) || !aligned(o_part, 16) || !aligned(lse_part, 4) || !aligned(workspace, 16))
+    return APB_ERR_MISALIGNED;
+  if (has_cache && (!aligned(k_cache, 16) || !aligned(v_cache, 16))) return APB_ERR_MISALIGNED;
+  if (app && (!aligned(k_new, 16) || !aligned(v_new, 16))) return APB_ERR_MISALIGNED;
+  apb::DecodeArgs a = decode_args(p);
+  const uint64_t need = apb::plan_decode(a).workspace_bytes;
+  if (workspace_bytes < need) return APB_ERR_BAD_SHAPE;
+  const int64_t d = p->head_dim, rows = (int64_t)p->n_q_heads * p->n_new;
+  const int64_t cache_bytes = has_cache ? (int64_t)p->n_kv_heads * p->cache_len * d * 2 : 0;
+  const int64_t new_bytes = app ? (int64_t)p->n_kv_heads * p->n_new * d * 2 : 0;
+  const Range in[5] = {range_of(q, rows * d * 2), range_of(has_cache ? k_cache : nullptr, cache_bytes),
+                       range_of(has_cache ? v_cache : nullptr, cache_bytes),
+                       range_of(app ? k_new : nullptr, new_bytes),
+                       range_of(app ? v_new : nullptr, new_bytes)};
+  const Range out[3] = {range_of(o_part, rows * d * 4), range_of(lse_part, rows * 4),
+                        range_of(workspace, (int64_t)need)};
+  for (const Range& r : out)
+    for (const Range& i : in)
+      if (overlaps(r, i)) return APB_ERR_ALIAS;
+  if (overlaps(out[0], out[1]) || overlaps(out[0], out[2]) || overlaps(out[1], out[2]))
+    return APB_ERR_ALIAS;
+
+  float scale = softmax_scale;
+  if (!(scale > 0.f) || !isfinite(scale)) scale = 1.f / sqrtf((float)p->head_dim);
+  a.q = q;
+  a.kc = has_cache ? k_cache : nullptr;
+  a.vc = has_cache ? v_cache : nullptr;
+  a.kn = app ? k_new : nullptr;
+  a.vn = app ? v_new : nullptr;
+  a.o = o_part; a.lse = lse_part;
+  a.workspace = static_cast<float*>(workspace);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const hipError_t e = apb::launch_decode(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    set_last_error(e);
+    return APB_ERR_HIP;
+  }
+  return APB_OK;
+}
+
+apb_status_t apb_merge_partials(int32_t n_parts, int32_t rows, int32_t head_dim,
+                                const float* o_parts, const float* lse_parts, uint16_t* o,
+                                float* lse, void* stream) {
+  if (n_parts < 1 || rows < 0 || head_dim < 1) return APB_ERR_BAD_SHAPE;
+  if ((int64_t)n_parts * rows > kMaxRows) return APB_ERR_BAD_SHAPE;
+  if (head_dim != 64 && head_dim != 128) return APB_ERR_UNSUPPORTED;
+  if (rows == 0) return APB_OK;
+  if (!o_parts || !lse_parts || !o) return APB_ERR_NULL_POINTER;
+  if (!aligned(o_parts, 16) || !aligned(lse_parts, 4) || !aligned(o, 16) ||
+      (lse && !aligned(lse, 4)))
+    return APB_ERR_MISALIGNED;
+  const int64_t d = head_dim;
+  const Range in[2] = {range_of(o_parts, (int64_t)n_parts * rows * d * 4),
+                       range_of(lse_parts, (int64_t)n_parts * rows * 4)};
+  const Range out[2] = {range_of(o, (int64_t)rows * d * 2), range_of(lse, lse ? (int64_t)rows * 4 : 0)};
+  for (const Range& r : out)
+    for (const Range& i : in)
+      if (overlaps(r, i)) return APB_ERR_ALIAS;
+  if (overlaps(out[0], out[1])) return APB_ERR_ALIAS;
+  apb::MergeArgs a;
+  a.o_parts = o_parts; a.lse_parts = lse_parts; a.o = o; a.lse = lse;
+  a.n_parts = n_parts; a.rows = rows; a.head_dim = head_dim;
+  const hipError_t e = apb::launch_merge(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    set_last_error(e);
+    return APB_ERR_HIP;
+  }
+  return APB_OK;
+}
+
 }  // extern "C"

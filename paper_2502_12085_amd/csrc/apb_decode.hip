@@ -1,0 +1,344 @@
+// Decoding stage of APB (stage 2, Alg. 3) for gfx950: one host's exact
+// attention of the new tokens against its KV cache, returned with the
+// per-row LSE, and MergeScore, the exact combination of such partial results.
+//
+// Partial attention.  Rows are (query head, new token) pairs; the rows of one
+// GQA group are contiguous ([n_q][n_new] order), so a 32-row block of one KV
+// head shares every key.  Keys are the host's cache followed, on the last
+// host, by the new tokens' own keys (new token j sees the cache and new
+// tokens 0..j).  The work is memory-bound (every cached key/value is read
+// once and used by at most g * n_new rows), so the key range is split over
+// many one-wave workgroups (flash-decoding): workgroup (s, kv, rb) runs an
+// online softmax over its share of the keys for one 32-row block and writes
+// its unnormalised-free partial (O / l, lse) in fp32 to a caller-provided
+// workspace; the merge kernel then combines the splits into the host's
+// partial.
+//  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (32 keys on M, 32 rows on N).
+//  * K and V blocks (32 keys) are copied HBM -> LDS with global_load_lds_dwordx4
+//    into XOR-swizzled row-major tiles, double buffered, so the copies of
+//    block b+1 fly while block b is computed.  K is read back with
+//    ds_read_b128 as the A operand of S^T; V is read back transposed with
+//    ds_read_b64_tr_b16 as the A operand of O^T = V^T P^T, and P comes
+//    straight from the S^T accumulator layout.
+//  * Online softmax in base 2 in fp32, P rounded to bf16 for the PV MFMA.
+//
+// MergeScore.  lse = m + ln sum_p exp(lse_p - m), A = sum_p exp(lse_p - lse)
+// A_p, one thread per row and four output dims; parts with lse = -inf add
+// nothing; a row with no part left gets A = 0, lse = -inf.
+#include <math.h>
+
+#include "apb_internal.h"
+
+namespace apb {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+
+constexpr int kRows = 32;   // rows per workgroup (the MFMA N side)
+constexpr int kKeys = 32;   // keys per block (the MFMA M side)
+
+struct DecParams {
+  const uint16_t* q;
+  const uint16_t* kc;
+  const uint16_t* vc;
+  const uint16_t* kn;
+  const uint16_t* vn;
+  float* part_o;    // [n_split][n_q * n_new][d]
+  float* part_lse;  // [n_split][n_q * n_new]
+  int Lc, n_new, append, n_kv, R, rows_total, blocks_per_split;
+  float scale_log2;
+};
+
+__device__ __forceinline__ float half_swap(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float((threadIdx.x & 63) < 32 ? r[1] : r[0]);
+}
+
+// LDS tile swizzles: 16-byte chunk c of key row r sits at chunk c ^ swz(r).
+// K: the 32 rows one ds_read_b128 pass touches hit distinct chunk slots;
+// V: the transposing reads of 4 rows x 4 chunks hit 16 distinct slots.
+template <int D>
+__device__ __forceinline__ int k_swz(int r) { return r & (D / 8 - 1); }
+template <int D>
+__device__ __forceinline__ int v_swz(int r) { return (4 * (r & 3)) & (D / 8 - 1); }
+
+__device__ __forceinline__ uint32_t lds_offset(const uint16_t* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint16_t*)p;
+}
+
+// Key / value row c of the concatenation [cache; new] of KV head kvh.
+template <int D>
+__device__ __forceinline__ const uint16_t* kv_row(const DecParams& p, const uint16_t* cache,
+                                                  const uint16_t* fresh, int kvh, int c) {
+  return c < p.Lc ? cache + ((size_t)kvh * p.Lc + c) * D
+                  : fresh + ((size_t)kvh * p.n_new + (c - p.Lc)) * D;
+}
+
+template <int D>
+__global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
+  constexpr int NKC = D / 16;                // MFMA k-steps over head_dim
+  constexpr int NDB = D / 32;                // 32-dim blocks of O^T
+  constexpr int KCH = D / 8;                 // 16-byte chunks per row
+  constexpr int PIECES = kKeys * D / 512;    // 1 KiB copies per V tile
+  constexpr int ROWS_PER_PIECE = 512 / D;
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKeys * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kKeys * D];
+
+  const int lane = threadIdx.x, n = lane & 31, h = lane >> 5;
+  const int split = blockIdx.x, kvh = blockIdx.y, rb = blockIdx.z;
+  const int Ltot = p.Lc + (p.append ? p.n_new : 0);
+  const int nblk = (Ltot + kKeys - 1) / kKeys;
+  const int b0 = split * p.blocks_per_split;
+  const int b1 = min(b0 + p.blocks_per_split, nblk);
+
+  // this lane's row (MFMA column n): query head kvh*g + rho / n_new, token rho % n_new
+  const int rho = rb * kRows + n;
+  const bool row_ok = rho < p.R;
+  const int tok = row_ok ? rho % p.n_new : 0;
+  const int vis = p.Lc + (p.append ? tok + 1 : 0);  // keys this row sees
+  const size_t grow = (size_t)kvh * p.R + (row_ok ? rho : 0);  // row in [n_q * n_new]
+
+  bf16x8 qreg[NKC];  // Q^T operand: row rho, dims 16*kc + 8*h .. +7
+  {
+    const unsigned keep = row_ok ? ~0u : 0u;
+    const uint16_t* qrow = p.q + grow * D;
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 16 * kc + 8 * h);
+      qreg[kc] = __builtin_bit_cast(bf16x8, raw & keep);
+    }
+  }
+
+  // per-lane copy slots: piece j covers key rows j*ROWS_PER_PIECE .. + ROWS_PER_PIECE-1
+  // (lane / KCH picks the row, lane % KCH the swizzled chunk slot)
+  const int cp_row0 = lane / KCH, cp_slot = lane % KCH;
+  // K operand lane offset: key row n, chunk (2*kc + h) ^ k_swz(n) sits at
+  // k_lane ^ (32*kc) (see the prefill kernel)
+  const uint32_t k_lane = (uint32_t)(n * 2 * D + 16 * ((h ^ n) & 1) + 16 * (n & (KCH - 2)));
+  // transposing-read lane base (see the prefill kernel for the derivation)
+  uint32_t v_lane;
+  {
+    const int g = lane >> 4, sl = lane & 15;
+    const int row = 4 * (g >> 1) + (sl >> 2);
+    v_lane = (uint32_t)(row * 2 * D + 64 * (row & (NDB - 1)) +
+                        16 * (2 * (g & 1) + ((sl & 3) >> 1)) + 8 * (sl & 1));
+  }
+
+  // K and V tiles of block b -> LDS buffer buf (16-byte copies, lane l's
+  // bytes land at M0 + 16*l; rows past the last key repeat it and are masked)
+  auto load_block = [&](int b, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < PIECES; ++j) {
+      const int row = j * ROWS_PER_PIECE + cp_row0;
+      const int c = min(b * kKeys + row, Ltot - 1);
+      const uint16_t* ks = kv_row<D>(p, p.kc, p.kn, kvh, c) + 8 * (cp_slot ^ k_swz<D>(row));
+      const uint16_t* vs = kv_row<D>(p, p.vc, p.vn, kvh, c) + 8 * (cp_slot ^ v_swz<D>(row));
+      const uint32_t kd = __builtin_amdgcn_readfirstlane(lds_offset(&k_lds[buf][j * 512]));
+      const uint32_t vd = __builtin_amdgcn_readfirstlane(lds_offset(&v_lds[buf][j * 512]));
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(ks), "s"(kd)
+                   : "memory", "m0");
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(vs), "s"(vd)
+                   : "memory", "m0");
+    }
+  };
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  if (b0 < b1) load_block(b0, 0);
+  for (int b = b0; b < b1; ++b) {
+    const int buf = (b - b0) & 1;
+    // block b has landed (this wave is the workgroup: its own wait suffices);
+    // then block b+1 goes out into the other buffer, whose reads ended with
+    // the previous iteration
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (b + 1 < b1) load_block(b + 1, buf ^ 1);
+    const uint32_t kl = lds_offset(k_lds[buf]);
+    bf16x8 kop[NKC];
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc)
+      kop[kc] = *(const lds_bf16x8*)(uintptr_t)(kl + (k_lane ^ (32u * (uint32_t)kc)));
+    f32x16 s = {};
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qreg[kc], s, 0, 0, 0);
+    // mask: element r of this lane is key b*32 + 8*(r/4) + 4*h + r%4 of row rho
+    const int c0 = b * kKeys;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
+      if (c >= vis) s[r] = -INFINITY;
+    }
+    float mx = s[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+    mx = fmaxf(mx, half_swap(mx));
+    const float m_new = fmaxf(m_run, mx * p.scale_log2);
+    bf16x8 pb[2];
+    if (m_new == -INFINITY) {  // nothing visible yet in this row
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pb[r >> 3][r & 7] = (__bf16)0.f;
+    } else {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // m_run = -inf gives 0
+      m_run = m_new;
+      float rs = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -m_new));
+        rs += e;
+        pb[r >> 3][r & 7] = (__bf16)e;
+      }
+      l_run = l_run * alpha + rs;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    }
+    // O^T += V^T P^T: the V tile of block b is in LDS (waited for above)
+    const uint32_t vb = lds_offset(v_lds[buf]);
+#pragma unroll
+    for (int cst = 0; cst < 2; ++cst)
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const uint32_t x = vb + (v_lane ^ (64u * (uint32_t)db));
+        i16x4 part[2];
+#pragma unroll
+        for (int rd = 0; rd < 2; ++rd)
+          part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(uintptr_t)(x + (uint32_t)((16 * cst + 8 * rd) * 2 * D)));
+        const bf16x8 a = __builtin_bit_cast(
+            bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[cst], oacc[db], 0, 0, 0);
+      }
+    // every lane's LDS reads of this buffer are done before it is refilled
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+
+  if (!row_ok) return;
+  const float l_tot = l_run + half_swap(l_run);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  float* orow = p.part_o + ((size_t)split * p.rows_total + grow) * D;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      f32x4 w;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = oacc[db][4 * g + i] * inv;
+      *reinterpret_cast<f32x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
+    }
+  if (h == 0)
+    p.part_lse[(size_t)split * p.rows_total + grow] =
+        l_tot > 0.f ? m_run * 0.69314718055994531f + logf(l_tot) : -INFINITY;
+}
+
+// MergeScore over n_parts partial results of `rows` rows.
+template <typename OutT>
+__global__ void __launch_bounds__(256) merge_kernel(int n_parts, int rows, int d,
+                                                    const float* __restrict__ o_parts,
+                                                    const float* __restrict__ lse_parts,
+                                                    OutT* __restrict__ o, float* __restrict__ lse) {
+  const int tpr = d / 4;  // threads per row
+  const int row = blockIdx.x * (256 / tpr) + threadIdx.x / tpr;
+  const int c = (threadIdx.x % tpr) * 4;
+  if (row >= rows) return;
+  float m = -INFINITY;
+  for (int q = 0; q < n_parts; ++q) m = fmaxf(m, lse_parts[(size_t)q * rows + row]);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float tot = 0.f;
+  if (m != -INFINITY) {
+    for (int q = 0; q < n_parts; ++q) {
+      const float w = __expf(lse_parts[(size_t)q * rows + row] - m);
+      if (w == 0.f) continue;
+      const f32x4 x = *reinterpret_cast<const f32x4*>(o_parts + ((size_t)q * rows + row) * d + c);
+      acc += w * x;
+      tot += w;
+    }
+  }
+  const float inv = tot > 0.f ? 1.f / tot : 0.f;
+  if constexpr (sizeof(OutT) == 4) {
+    *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(o) + (size_t)row * d + c) = acc * inv;
+  } else {
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    bf16x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (__bf16)(acc[i] * inv);
+    *reinterpret_cast<bf16x4*>(reinterpret_cast<uint16_t*>(o) + (size_t)row * d + c) = w;
+  }
+  if (lse && c == 0) lse[row] = tot > 0.f ? m + logf(tot) : -INFINITY;
+}
+
+template <typename OutT>
+hipError_t launch_merge_t(int n_parts, int rows, int d, const float* o_parts,
+                          const float* lse_parts, OutT* o, float* lse, hipStream_t stream) {
+  if (rows == 0) return hipSuccess;
+  const int rows_per_block = 256 / (d / 4);
+  const dim3 grid((unsigned)((rows + rows_per_block - 1) / rows_per_block));
+  hipLaunchKernelGGL(merge_kernel<OutT>, grid, dim3(256), 0, stream, n_parts, rows, d, o_parts,
+                     lse_parts, o, lse);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+DecodePlan plan_decode(const DecodeArgs& a) {
+  DecodePlan pl;
+  const int64_t keys = (int64_t)a.Lc + (a.append ? a.n_new : 0);
+  const int64_t nblk = (keys + kKeys - 1) / kKeys;
+  const int64_t R = (int64_t)(a.n_q / a.n_kv) * a.n_new;
+  const int64_t n_rb = (R + kRows - 1) / kRows;
+  // about 8 one-wave workgroups per CU, at least two key blocks each
+  const int64_t target = 2048;
+  int64_t n_split = target / (a.n_kv * n_rb);
+  if (n_split > nblk / 2) n_split = nblk / 2;
+  if (n_split < 1) n_split = 1;
+  int64_t bps = nblk > 0 ? (nblk + n_split - 1) / n_split : 0;
+  if (bps > 0) n_split = (nblk + bps - 1) / bps;
+  pl.n_split = (int)n_split;
+  pl.blocks_per_split = (int)bps;
+  pl.row_blocks = (int)n_rb;
+  const int64_t rows_total = (int64_t)a.n_q * a.n_new;
+  pl.workspace_bytes = (uint64_t)n_split * rows_total * (a.head_dim + 1) * 4;
+  return pl;
+}
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
+  const DecodePlan pl = plan_decode(a);
+  DecParams p;
+  p.q = a.q; p.kc = a.kc; p.vc = a.vc; p.kn = a.kn; p.vn = a.vn;
+  const int64_t rows_total = (int64_t)a.n_q * a.n_new;
+  p.part_o = a.workspace;
+  p.part_lse = a.workspace + (size_t)pl.n_split * rows_total * a.head_dim;
+  p.Lc = a.Lc; p.n_new = a.n_new; p.append = a.append; p.n_kv = a.n_kv;
+  p.R = (a.n_q / a.n_kv) * a.n_new;
+  p.rows_total = (int)rows_total;
+  p.blocks_per_split = pl.blocks_per_split;
+  p.scale_log2 = a.scale_log2;
+  const dim3 grid((unsigned)pl.n_split, (unsigned)a.n_kv, (unsigned)pl.row_blocks);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL(decode_partial_kernel<128>, grid, dim3(64), 0, stream, p);
+  else
+    hipLaunchKernelGGL(decode_partial_kernel<64>, grid, dim3(64), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_merge_t<float>(pl.n_split, (int)rows_total, a.head_dim, p.part_o, p.part_lse,
+                               a.o, a.lse, stream);
+}
+
+hipError_t launch_merge(const MergeArgs& a, hipStream_t stream) {
+  return launch_merge_t<uint16_t>(a.n_parts, a.rows, a.head_dim, a.o_parts, a.lse_parts, a.o,
+                                  a.lse, stream);
+}
+
+}  // namespace apb

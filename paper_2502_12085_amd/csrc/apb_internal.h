@@ -1,5 +1,6 @@
 // Internal launch interface between the C-ABI layer (apb_api.hip) and the
-// gfx950 kernels (apb_attention.hip, apb_compress.hip).  Not installed.
+// gfx950 kernels (apb_attention.hip, apb_compress.hip, apb_decode.hip).
+// Not installed.
 #ifndef APB_INTERNAL_H_
 #define APB_INTERNAL_H_
 
@@ -34,8 +35,43 @@ struct CompressArgs {
   int32_t n_kv, head_dim;
 };
 
+// One host's decoding-stage attention (Alg. 3), already validated.
+struct DecodeArgs {
+  const uint16_t* q;   // [n_q][n_new][d]
+  const uint16_t* kc;  // [n_kv][Lc][d], may be null when Lc == 0
+  const uint16_t* vc;
+  const uint16_t* kn;  // [n_kv][n_new][d], used when append
+  const uint16_t* vn;
+  float* o;            // [n_q][n_new][d]
+  float* lse;          // [n_q][n_new]
+  float* workspace;    // DecodePlan::workspace_bytes, 16-byte aligned
+  int32_t Lc, n_new, append;
+  int32_t n_q, n_kv, head_dim;
+  float scale_log2;
+};
+
+// How a decode call splits its keys; the workspace holds one fp32 partial
+// (O and LSE) per split and row.
+struct DecodePlan {
+  int n_split;
+  int blocks_per_split;
+  int row_blocks;
+  uint64_t workspace_bytes;
+};
+
+struct MergeArgs {
+  const float* o_parts;    // [n_parts][rows][d]
+  const float* lse_parts;  // [n_parts][rows]
+  uint16_t* o;             // [rows][d] bf16
+  float* lse;              // [rows], may be null
+  int32_t n_parts, rows, head_dim;
+};
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_compress(const CompressArgs& a, hipStream_t stream);
+DecodePlan plan_decode(const DecodeArgs& a);
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
 
 }  // namespace apb
 

@@ -165,3 +165,70 @@ def make_host_blocks(wl: Workload, seed: int = 0) -> list:
             sc = rng.standard_normal((p.n_kv_heads, p.local_len), dtype=np.float32)
         out.append(dict(k=k, v=v, scores=sc))
     return out
+
+
+# ----------------------------------------------------------- decoding stage
+@dataclasses.dataclass(frozen=True)
+class DecodeWorkload:
+    """One decoding step (Alg. 3) over H hosts: every host's cache is its
+    local block (Alg. 1 keeps K_h, V_h), the last host also appends the new
+    tokens' K/V."""
+
+    name: str
+    n_hosts: int
+    cache_len: int  # rows per host cache (the local block length l_b)
+    n_new: int      # new tokens this step
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    outlier_k: bool = False
+
+    @property
+    def rows(self) -> int:
+        return self.n_q_heads * self.n_new
+
+
+# The 128K Llama-8B-shaped layer after its prefill (H = 8 hosts of 16384
+# cached rows): one generated token, and the first step that feeds the
+# question tokens (64 of them here).
+DECODE_WORKLOADS = {
+    "tiny_decode": DecodeWorkload("tiny_decode", 4, 512, 3, 4, 1, 64),
+    "llama8b_128k_decode": DecodeWorkload("llama8b_128k_decode", 8, 16384, 1, 32, 8, 128,
+                                          outlier_k=True),
+    "llama8b_128k_question": DecodeWorkload("llama8b_128k_question", 8, 16384, 64, 32, 8, 128,
+                                            outlier_k=True),
+}
+
+
+def make_decode_case(n_q: int, n_kv: int, d: int, cache_lens, n_new: int, seed: int = 0,
+                     outlier_k: bool = False) -> dict:
+    """Inputs of one decoding step over len(cache_lens) hosts.
+
+    Streams: ``SeedSequence(seed).spawn(4 + 2*H)`` in the order Q, K_new,
+    V_new, outlier channels, then K and V of host 0, 1, ...  Returns ``q``
+    [n_q, n_new, d], ``k_new``/``v_new`` [n_kv, n_new, d], ``caches`` (list of
+    (k, v), each [n_kv, Lc_h, d]), all bf16 bits."""
+    H = len(cache_lens)
+    ss = np.random.SeedSequence(seed).spawn(4 + 2 * H)
+    cols = None
+    if outlier_k:
+        n_out = math.ceil(0.02 * d)
+        rng = np.random.default_rng(ss[3])
+        cols = np.stack([np.sort(rng.choice(d, n_out, replace=False)) for _ in range(n_kv)])
+    q = _normal_bf16(np.random.default_rng(ss[0]), (n_q, n_new, d))
+    k_new = _normal_bf16(np.random.default_rng(ss[1]), (n_kv, n_new, d), cols)
+    v_new = _normal_bf16(np.random.default_rng(ss[2]), (n_kv, n_new, d))
+    caches = []
+    for h, lc in enumerate(cache_lens):
+        kc = _normal_bf16(np.random.default_rng(ss[4 + 2 * h]), (n_kv, lc, d), cols)
+        vc = _normal_bf16(np.random.default_rng(ss[5 + 2 * h]), (n_kv, lc, d))
+        caches.append((kc, vc))
+    return dict(q=q, k_new=k_new, v_new=v_new, caches=caches)
+
+
+def make_decode_inputs(wl: DecodeWorkload, seed: int = 0, hosts=None) -> dict:
+    """``make_decode_case`` for a named workload; ``hosts`` limits how many
+    host caches are drawn (the first ones), e.g. 1 for the last host alone."""
+    h = wl.n_hosts if hosts is None else hosts
+    return make_decode_case(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, [wl.cache_len] * h,
+                            wl.n_new, seed, wl.outlier_k)

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(apb.EXPORTED)
     for name in declared:
         assert hasattr(L, name), name
-    assert apb.abi_version() == 1
+    assert apb.abi_version() == 2
 
 
 def _prob(**kw):
@@ -126,3 +126,84 @@ def test_binding_rejects_host_tensors():
     x = torch.zeros(4, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         apb.attention_fwd(inputs.WORKLOADS["tiny"].problem, x, x, x, x, x, x)
+
+
+# ------------------------------------------------------- decoding stage
+def _dprob(**kw):
+    base = dict(n_q_heads=8, n_kv_heads=2, head_dim=128, cache_len=1000, n_new=3, append_new=1)
+    base.update(kw)
+    return apb.DecodeProblem(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), 0),
+    (dict(append_new=0), 0),
+    (dict(cache_len=0), 0),
+    (dict(cache_len=-1), 2),
+    (dict(n_new=0), 2),
+    (dict(append_new=2), 2),
+    (dict(n_q_heads=6, n_kv_heads=4), 2),
+    (dict(n_kv_heads=0), 2),
+    (dict(head_dim=80), 3),
+    (dict(cache_len=1 << 30), 2),
+])
+def test_validate_decode(kw, code):
+    assert apb.validate_decode(_dprob(**kw)) == code
+
+
+def test_decode_workspace_size_is_shape_only():
+    # one fp32 partial (O and LSE) per split and row; more keys never need
+    # less scratch per row, and the size is a multiple of 16 bytes
+    rows = 8 * 3
+    sizes = []
+    for lc in (0, 1, 31, 32, 1000, 16384, 65536):
+        n = apb.decode_workspace_size(_dprob(cache_len=lc))
+        assert n > 0 and n % (rows * 129 * 4) == 0
+        sizes.append(n // (rows * 129 * 4))
+    assert sizes == sorted(sizes) and sizes[0] == 1
+    with pytest.raises(apb.ApbError):
+        apb.decode_workspace_size(_dprob(head_dim=80))
+    assert apb.lib().apb_decode_workspace_size(ctypes.byref(_dprob()), None) == 1
+
+
+DQ, DKC, DVC, DKN, DVN, DO, DL, WS = (A + i * (1 << 36) for i in range(8))
+
+
+def _dec(p, q=DQ, kc=DKC, vc=DVC, kn=DKN, vn=DVN, o=DO, lse=DL, ws=WS, ws_bytes=1 << 30):
+    return apb.lib().apb_decode_attention(ctypes.byref(p), q, kc, vc, kn, vn, o, lse, 0.0, ws,
+                                          ws_bytes, None)
+
+
+def test_decode_error_paths():
+    p = _dprob()
+    assert apb.lib().apb_decode_attention(None, DQ, DKC, DVC, DKN, DVN, DO, DL, 0.0, WS, 1 << 30,
+                                          None) == 1
+    assert _dec(p, q=None) == 1
+    assert _dec(p, lse=None) == 1            # MergeScore needs the LSE
+    assert _dec(p, ws=None) == 1
+    assert _dec(p, kc=None) == 1             # cache required when Lc > 0
+    assert _dec(p, kn=None) == 1             # new K/V required on the last host
+    assert _dec(_dprob(append_new=0), kn=None, vn=None) != 1
+    assert _dec(_dprob(cache_len=0), kc=None, vc=None) != 1
+    assert _dec(p, ws_bytes=16) == 2         # workspace too small
+    assert _dec(p, q=DQ + 8) == 4
+    assert _dec(p, o=DO + 4) == 4
+    assert _dec(p, ws=WS + 4) == 4
+    assert _dec(p, o=DQ) == 6
+    assert _dec(p, ws=DKC + 64) == 6
+    assert _dec(p, lse=DO + 16) == 6
+    assert _dec(_dprob(head_dim=80)) == 3
+
+
+def test_merge_error_paths():
+    L = apb.lib()
+    assert L.apb_merge_partials(0, 4, 128, DO, DL, DQ, WS, None) == 2
+    assert L.apb_merge_partials(2, -1, 128, DO, DL, DQ, WS, None) == 2
+    assert L.apb_merge_partials(2, 4, 96, DO, DL, DQ, WS, None) == 3
+    assert L.apb_merge_partials(2, 0, 128, None, None, None, None, None) == 0  # nothing to do
+    assert L.apb_merge_partials(2, 4, 128, None, DL, DQ, WS, None) == 1
+    assert L.apb_merge_partials(2, 4, 128, DO, DL, None, WS, None) == 1
+    assert L.apb_merge_partials(2, 4, 128, DO + 4, DL, DQ, WS, None) == 4
+    assert L.apb_merge_partials(2, 4, 128, DO, DL, DQ + 2, WS, None) == 4
+    assert L.apb_merge_partials(2, 4, 128, DO, DL, DO + 64, WS, None) == 6
+    assert L.apb_merge_partials(2, 4, 128, DO, DL, DQ, DL + 4, None) == 6
