@@ -80,6 +80,67 @@ def cpu_baseline(wl, inp, budget_s: float):
             "seconds": round(el, 3)}
 
 
+def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
+    """Decoding stage (Alg. 3) at the same layer shape: the last host's
+    partial attention over its cache plus the new tokens' K/V, and MergeScore
+    of the H hosts' partials (the other hosts' partials are synthetic).  HIP
+    events on the launch stream; inputs resident in HBM."""
+    import numpy as np
+    import torch
+    from paper_2502_12085_amd import apb, inputs
+
+    case = inputs.make_decode_inputs(wl, seed, hosts=1)
+    kc, vc = case["caches"][0]
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, dkc, dvc, kn, vn = dev(case["q"]), dev(kc), dev(vc), dev(case["k_new"]), dev(case["v_new"])
+    n_q, n_kv, d, n_new, lc, H = (wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.n_new,
+                                  wl.cache_len, wl.n_hosts)
+    rows = n_q * n_new
+    prob = apb.DecodeProblem(n_q, n_kv, d, lc, n_new, 1)
+    ws = torch.empty(apb.decode_workspace_size(prob), dtype=torch.uint8, device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    parts_o = torch.randn((H, rows, d), generator=g, device="cuda", dtype=torch.float32)
+    parts_l = torch.randn((H, rows), generator=g, device="cuda", dtype=torch.float32)
+    o = torch.empty((rows, d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((rows,), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        apb.decode_attention(prob, q, dkc, dvc, kn, vn, parts_o[H - 1].view(n_q, n_new, d),
+                             parts_l[H - 1].view(n_q, n_new), ws, 0.0, stream)
+        e1.record(stream)
+        apb.merge_partials(parts_o, parts_l, o, lse, stream)
+
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t_dec, t_mrg = [], []
+    for _ in range(steps):
+        e0.record(stream)
+        step()
+        e2.record(stream)
+        e2.synchronize()
+        t_dec.append(e0.elapsed_time(e1))
+        t_mrg.append(e1.elapsed_time(e2))
+    dec_us = 1e3 * sorted(t_dec)[len(t_dec) // 2]
+    mrg_us = 1e3 * sorted(t_mrg)[len(t_mrg) // 2]
+    keys = lc + n_new
+    dec_bytes = 2 * rows * d + 2 * 2 * n_kv * keys * d + 4 * rows * d + 4 * rows
+    mrg_bytes = H * rows * (d + 1) * 4 + rows * d * 2 + rows * 4
+    return {"workload": wl.name, "n_hosts": H, "cache_len": lc, "n_new": n_new,
+            "n_q_heads": n_q, "n_kv_heads": n_kv, "head_dim": d,
+            "decode_us": round(dec_us, 2), "decode_algorithmic_bytes": dec_bytes,
+            "decode_gbs": round(dec_bytes / (dec_us * 1e-6) / 1e9, 1),
+            "decode_hbm_frac": round(dec_bytes / (dec_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "merge_us": round(mrg_us, 2), "merge_algorithmic_bytes": mrg_bytes,
+            "kernel": "decode_partial_kernel<128> + merge_kernel",
+            "bound": "hbm", "timing": f"median of {steps} launches, HIP events"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -90,6 +151,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stage2", action="store_true",
+                    help="skip the decoding-stage (Alg. 3) measurement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (for scaling "
                          "the HBM byte counters) and exit")
@@ -207,6 +270,9 @@ def main():
                           "a800_implied_tflops": round(flops / 34.07e-3 / 1e12, 1),
                           "note": "8xA800 per-block breakdown at 128K; another machine"},
     }
+    if not args.no_stage2:
+        result["stage2"] = [bench_stage2(inputs.DECODE_WORKLOADS[n], max(args.steps, 20), 5)
+                            for n in ("llama8b_128k_decode", "llama8b_128k_question")]
     if not args.no_cpu_baseline:
         print("# timing the fp64 oracle on the host cores", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(wl, inp, args.cpu_budget)

@@ -15,16 +15,16 @@
 // partial.
 //  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (32 keys on M, 32 rows on N).
 //  * K and V blocks (32 keys) are copied HBM -> LDS with global_load_lds_dwordx4
-//    into XOR-swizzled row-major tiles, double buffered, so the copies of
-//    block b+1 fly while block b is computed.  K is read back with
+//    into XOR-swizzled row-major tiles, a three-stage ring, so the copies
+//    of blocks b+1 and b+2 fly while block b is computed.  K is read back with
 //    ds_read_b128 as the A operand of S^T; V is read back transposed with
 //    ds_read_b64_tr_b16 as the A operand of O^T = V^T P^T, and P comes
 //    straight from the S^T accumulator layout.
 //  * Online softmax in base 2 in fp32, P rounded to bf16 for the PV MFMA.
 //
 // MergeScore.  lse = m + ln sum_p exp(lse_p - m), A = sum_p exp(lse_p - lse)
-// A_p, one thread per row and four output dims; parts with lse = -inf add
-// nothing; a row with no part left gets A = 0, lse = -inf.
+// A_p with m the largest lse_p; parts with lse = -inf add nothing; a row
+// with no part left gets A = 0, lse = -inf.
 #include <math.h>
 
 #include "apb_internal.h"
@@ -42,6 +42,8 @@ typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
 constexpr int kRows = 32;   // rows per workgroup (the MFMA N side)
 constexpr int kKeys = 32;   // keys per block (the MFMA M side)
+constexpr int kRing = 3;    // LDS stages of K and V blocks per workgroup
+constexpr int kWgPerCu = 3; // workgroups per CU (LDS: 3 x 48 KiB at d = 128)
 
 struct DecParams {
   const uint16_t* q;
@@ -86,10 +88,11 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
   constexpr int NKC = D / 16;                // MFMA k-steps over head_dim
   constexpr int NDB = D / 32;                // 32-dim blocks of O^T
   constexpr int KCH = D / 8;                 // 16-byte chunks per row
-  constexpr int PIECES = kKeys * D / 512;    // 1 KiB copies per V tile
+  constexpr int PIECES = kKeys * D / 512;    // 1 KiB copies per K or V tile
+  static_assert(PIECES == 4 || PIECES == 8, "copy unrolling below");
   constexpr int ROWS_PER_PIECE = 512 / D;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKeys * D];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kKeys * D];
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kRing][kKeys * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kRing][kKeys * D];
 
   const int lane = threadIdx.x, n = lane & 31, h = lane >> 5;
   const int split = blockIdx.x, kvh = blockIdx.y, rb = blockIdx.z;
@@ -116,8 +119,8 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
     }
   }
 
-  // per-lane copy slots: piece j covers key rows j*ROWS_PER_PIECE .. + ROWS_PER_PIECE-1
-  // (lane / KCH picks the row, lane % KCH the swizzled chunk slot)
+  // per-lane copy slots: piece j (1 KiB) covers key rows j*ROWS_PER_PIECE ..
+  // + ROWS_PER_PIECE-1 (lane / KCH picks the row, lane % KCH the chunk slot)
   const int cp_row0 = lane / KCH, cp_slot = lane % KCH;
   // K operand lane offset: key row n, chunk (2*kc + h) ^ k_swz(n) sits at
   // k_lane ^ (32*kc) (see the prefill kernel)
@@ -131,21 +134,63 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
                         16 * (2 * (g & 1) + ((sl & 3) >> 1)) + 8 * (sl & 1));
   }
 
-  // K and V tiles of block b -> LDS buffer buf (16-byte copies, lane l's
-  // bytes land at M0 + 16*l; rows past the last key repeat it and are masked)
-  auto load_block = [&](int b, int buf) __attribute__((always_inline)) {
+  // K and V tiles of block b -> LDS buffer buf.  global_load_lds_dwordx4
+  // puts lane l's 16 bytes at M0 + inst_offset + 16*l and reads them from
+  // saddr + voffset + inst_offset, so a block inside one segment (cache or
+  // new rows) takes one scalar base and one M0 per tile; lane offsets
+  // (less the piece's KiB) are fixed per lane.  A block that straddles the
+  // cache end or the last key looks its rows up one by one (rows past the
+  // last key repeat it and are masked).
+  uint32_t k_off[PIECES], v_off[PIECES];
 #pragma unroll
-    for (int j = 0; j < PIECES; ++j) {
-      const int row = j * ROWS_PER_PIECE + cp_row0;
-      const int c = min(b * kKeys + row, Ltot - 1);
-      const uint16_t* ks = kv_row<D>(p, p.kc, p.kn, kvh, c) + 8 * (cp_slot ^ k_swz<D>(row));
-      const uint16_t* vs = kv_row<D>(p, p.vc, p.vn, kvh, c) + 8 * (cp_slot ^ v_swz<D>(row));
-      const uint32_t kd = __builtin_amdgcn_readfirstlane(lds_offset(&k_lds[buf][j * 512]));
-      const uint32_t vd = __builtin_amdgcn_readfirstlane(lds_offset(&v_lds[buf][j * 512]));
-      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(ks), "s"(kd)
-                   : "memory", "m0");
-      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(vs), "s"(vd)
-                   : "memory", "m0");
+  for (int j = 0; j < PIECES; ++j) {
+    const int row = j * ROWS_PER_PIECE + cp_row0;
+    // the instruction offset is 13-bit signed: pieces 4..7 use M0 + 4 KiB
+    k_off[j] = 2u * (uint32_t)(row * D + 8 * (cp_slot ^ k_swz<D>(row))) - 1024u * (j & 3);
+    v_off[j] = 2u * (uint32_t)(row * D + 8 * (cp_slot ^ v_swz<D>(row))) - 1024u * (j & 3);
+  }
+  auto load_block = [&](int b, int buf) __attribute__((always_inline)) {
+    const int c0 = b * kKeys;
+    const uint32_t kd = __builtin_amdgcn_readfirstlane(lds_offset(k_lds[buf]));
+    const uint32_t vd = __builtin_amdgcn_readfirstlane(lds_offset(v_lds[buf]));
+    const bool in_cache = c0 + kKeys <= p.Lc;
+    const bool in_new = c0 >= p.Lc && c0 + kKeys <= Ltot;
+    if (in_cache || in_new) {
+      const size_t r0 = in_cache ? (size_t)kvh * p.Lc + c0 : (size_t)kvh * p.n_new + (c0 - p.Lc);
+      const uint16_t* kb = (in_cache ? p.kc : p.kn) + r0 * D;
+      const uint16_t* vb = (in_cache ? p.vc : p.vn) + r0 * D;
+#define APB_DEC_PIECE(J, OFFS, BASE)                                                     \
+  asm volatile("global_load_lds_dwordx4 %0, %1 offset:" #J ::"v"(OFFS[(J) / 1024 + q4]), \
+               "s"(BASE)                                                                 \
+               : "memory")
+#pragma unroll
+      for (int q4 = 0; q4 < PIECES; q4 += 4) {
+        asm volatile("s_mov_b32 m0, %0" ::"s"(kd + 1024u * q4) : "memory");
+        APB_DEC_PIECE(0, k_off, kb);
+        APB_DEC_PIECE(1024, k_off, kb);
+        APB_DEC_PIECE(2048, k_off, kb);
+        APB_DEC_PIECE(3072, k_off, kb);
+        asm volatile("s_mov_b32 m0, %0" ::"s"(vd + 1024u * q4) : "memory");
+        APB_DEC_PIECE(0, v_off, vb);
+        APB_DEC_PIECE(1024, v_off, vb);
+        APB_DEC_PIECE(2048, v_off, vb);
+        APB_DEC_PIECE(3072, v_off, vb);
+      }
+#undef APB_DEC_PIECE
+    } else {
+#pragma unroll
+      for (int j = 0; j < PIECES; ++j) {
+        const int row = j * ROWS_PER_PIECE + cp_row0;
+        const int c = min(c0 + row, Ltot - 1);
+        const uint16_t* ks = kv_row<D>(p, p.kc, p.kn, kvh, c) + 8 * (cp_slot ^ k_swz<D>(row));
+        const uint16_t* vs = kv_row<D>(p, p.vc, p.vn, kvh, c) + 8 * (cp_slot ^ v_swz<D>(row));
+        asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(ks),
+                     "s"(kd + 1024u * j)
+                     : "memory");
+        asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(vs),
+                     "s"(vd + 1024u * j)
+                     : "memory");
+      }
     }
   };
 
@@ -156,14 +201,22 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
+  // three-stage ring: blocks b+1 and b+2 fly while block b is computed
   if (b0 < b1) load_block(b0, 0);
+  if (b0 + 1 < b1) load_block(b0 + 1, 1);
   for (int b = b0; b < b1; ++b) {
-    const int buf = (b - b0) & 1;
-    // block b has landed (this wave is the workgroup: its own wait suffices);
-    // then block b+1 goes out into the other buffer, whose reads ended with
-    // the previous iteration
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (b + 1 < b1) load_block(b + 1, buf ^ 1);
+    const int buf = (b - b0) % kRing;
+    // block b has landed once at most block b+1's copies are outstanding
+    // (this wave is the workgroup: its own wait suffices); then block b+2
+    // goes into the stage block b-1 used, whose reads ended with the
+    // previous iteration
+    if (b + 1 < b1) {
+      if constexpr (PIECES == 8) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    if (b + 2 < b1) load_block(b + 2, (b - b0 + 2) % kRing);
     const uint32_t kl = lds_offset(k_lds[buf]);
     bf16x8 kop[NKC];
 #pragma unroll
@@ -243,28 +296,68 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
         l_tot > 0.f ? m_run * 0.69314718055994531f + logf(l_tot) : -INFINITY;
 }
 
-// MergeScore over n_parts partial results of `rows` rows.
+// MergeScore over n_parts partial results of `rows` rows: one workgroup per
+// row.  The d/4 threads of a group cover the row's d outputs (four each) and
+// the 256/(d/4) groups split the parts among themselves, so both many parts
+// (the splits of one decode call) and few parts with many rows (the hosts of
+// a decoding step) keep loads in flight; the groups' sums meet in LDS.
 template <typename OutT>
 __global__ void __launch_bounds__(256) merge_kernel(int n_parts, int rows, int d,
                                                     const float* __restrict__ o_parts,
                                                     const float* __restrict__ lse_parts,
                                                     OutT* __restrict__ o, float* __restrict__ lse) {
-  const int tpr = d / 4;  // threads per row
-  const int row = blockIdx.x * (256 / tpr) + threadIdx.x / tpr;
-  const int c = (threadIdx.x % tpr) * 4;
-  if (row >= rows) return;
+  __shared__ float red[8];
+  __shared__ __attribute__((aligned(16))) float acc_lds[256 * 4];
+  __shared__ float tot_lds[64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = blockIdx.x;
+  const int tpr = d / 4, G = 256 / tpr;
+  const int grp = tid / tpr, c = (tid % tpr) * 4;
+  const float* lrow = lse_parts + row;
+
+  // 1. m = max over the parts' lse
   float m = -INFINITY;
-  for (int q = 0; q < n_parts; ++q) m = fmaxf(m, lse_parts[(size_t)q * rows + row]);
+  for (int q = tid; q < n_parts; q += 256) m = fmaxf(m, lrow[(size_t)q * rows]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if (lane == 0) red[wave] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+
+  // 2. this group's parts, four loads in flight per thread
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float tot = 0.f;
   if (m != -INFINITY) {
-    for (int q = 0; q < n_parts; ++q) {
-      const float w = __expf(lse_parts[(size_t)q * rows + row] - m);
-      if (w == 0.f) continue;
-      const f32x4 x = *reinterpret_cast<const f32x4*>(o_parts + ((size_t)q * rows + row) * d + c);
-      acc += w * x;
-      tot += w;
+    int q = grp;
+    for (; q + 3 * G < n_parts; q += 4 * G) {
+      float w[4];
+      f32x4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        w[u] = lrow[(size_t)(q + u * G) * rows];
+        x[u] = *reinterpret_cast<const f32x4*>(o_parts + ((size_t)(q + u * G) * rows + row) * d + c);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float e = __expf(w[u] - m);  // 0 for an empty part (lse = -inf)
+        acc += e * x[u];
+        tot += e;
+      }
     }
+    for (; q < n_parts; q += G) {
+      const float e = __expf(lrow[(size_t)q * rows] - m);
+      acc += e * *reinterpret_cast<const f32x4*>(o_parts + ((size_t)q * rows + row) * d + c);
+      tot += e;
+    }
+  }
+  // 3. sum over groups
+  *reinterpret_cast<f32x4*>(&acc_lds[4 * tid]) = acc;
+  if (tid % tpr == 0) tot_lds[grp] = tot;
+  __syncthreads();
+  if (grp != 0) return;
+  for (int g2 = 1; g2 < G; ++g2) {
+    acc += *reinterpret_cast<const f32x4*>(&acc_lds[4 * (g2 * tpr + tid)]);
+    tot += tot_lds[g2];
   }
   const float inv = tot > 0.f ? 1.f / tot : 0.f;
   if constexpr (sizeof(OutT) == 4) {
@@ -276,17 +369,15 @@ __global__ void __launch_bounds__(256) merge_kernel(int n_parts, int rows, int d
     for (int i = 0; i < 4; ++i) w[i] = (__bf16)(acc[i] * inv);
     *reinterpret_cast<bf16x4*>(reinterpret_cast<uint16_t*>(o) + (size_t)row * d + c) = w;
   }
-  if (lse && c == 0) lse[row] = tot > 0.f ? m + logf(tot) : -INFINITY;
+  if (lse && tid == 0) lse[row] = tot > 0.f ? m + logf(tot) : -INFINITY;
 }
 
 template <typename OutT>
 hipError_t launch_merge_t(int n_parts, int rows, int d, const float* o_parts,
                           const float* lse_parts, OutT* o, float* lse, hipStream_t stream) {
   if (rows == 0) return hipSuccess;
-  const int rows_per_block = 256 / (d / 4);
-  const dim3 grid((unsigned)((rows + rows_per_block - 1) / rows_per_block));
-  hipLaunchKernelGGL(merge_kernel<OutT>, grid, dim3(256), 0, stream, n_parts, rows, d, o_parts,
-                     lse_parts, o, lse);
+  hipLaunchKernelGGL(merge_kernel<OutT>, dim3((unsigned)rows), dim3(256), 0, stream, n_parts, rows,
+                     d, o_parts, lse_parts, o, lse);
   return hipGetLastError();
 }
 
@@ -298,8 +389,8 @@ DecodePlan plan_decode(const DecodeArgs& a) {
   const int64_t nblk = (keys + kKeys - 1) / kKeys;
   const int64_t R = (int64_t)(a.n_q / a.n_kv) * a.n_new;
   const int64_t n_rb = (R + kRows - 1) / kRows;
-  // about 8 one-wave workgroups per CU, at least two key blocks each
-  const int64_t target = 2048;
+  // one round of workgroups at kWgPerCu per CU, at least two key blocks each
+  const int64_t target = 256 * kWgPerCu;
   int64_t n_split = target / (a.n_kv * n_rb);
   if (n_split > nblk / 2) n_split = nblk / 2;
   if (n_split < 1) n_split = 1;
