@@ -1,5 +1,6 @@
 /*
- * apb.h -- C ABI of one host's share of APB prefill attention on MI355X.
+ * apb.h -- C ABI of one host's share of APB attention on MI355X: the prefill
+ * hot path and the decoding stage.
  *
  * APB (Accelerating distributed long-context inference by Passing compressed
  * context Blocks) splits a long document across H hosts.  Host h holds an
