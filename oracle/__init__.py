@@ -21,3 +21,9 @@ from .decode_oracle import (  # noqa: F401
     stage2_ref,
     decode_bytes,
 )
+from .scorer_oracle import (  # noqa: F401
+    scorer_features,
+    silu,
+    retaining_scores_ref,
+    scorer_flops,
+)

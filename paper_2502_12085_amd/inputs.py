@@ -232,3 +232,30 @@ def make_decode_inputs(wl: DecodeWorkload, seed: int = 0, hosts=None) -> dict:
     h = wl.n_hosts if hosts is None else hosts
     return make_decode_case(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, [wl.cache_len] * h,
                             wl.n_new, seed, wl.outlier_k)
+
+
+# ----------------------------------------------------- retaining-head scorer
+SCORER_HIDDEN = 1024  # intermediate size of the retaining heads (App. B)
+
+
+def make_scorer_weights(n_q: int, n_kv: int, head_dim: int, hidden: int = SCORER_HIDDEN,
+                        seed: int = 0) -> dict:
+    """Synthetic retaining-head weights (the trained ones are not available).
+
+    Streams ``SeedSequence(seed + 2000).spawn(4)``: W1 bf16 bits [hidden,
+    (n_q + 2 n_kv) d] ~ N(0, 1/features), b1 fp32 [hidden] ~ N(0, 0.1^2),
+    W2 fp32 [n_kv, hidden] ~ N(0, 1/hidden), b2 fp32 [n_kv] ~ N(0, 0.1^2),
+    so that with N(0, 1) inputs the hidden pre-activations and the scores
+    are of order one."""
+    feats = (n_q + 2 * n_kv) * head_dim
+    ss = np.random.SeedSequence(seed + 2000).spawn(4)
+    r = [np.random.default_rng(s) for s in ss]
+    w1 = np.empty((hidden, feats), np.uint16)
+    for j in range(hidden):
+        w1[j] = f32_to_bf16_bits(r[0].standard_normal(feats, dtype=np.float32)
+                                 * np.float32(1.0 / math.sqrt(feats)))
+    b1 = (r[1].standard_normal(hidden, dtype=np.float32) * np.float32(0.1))
+    w2 = (r[2].standard_normal((n_kv, hidden), dtype=np.float32)
+          * np.float32(1.0 / math.sqrt(hidden)))
+    b2 = (r[3].standard_normal(n_kv, dtype=np.float32) * np.float32(0.1))
+    return dict(w1=w1, b1=b1, w2=w2, b2=b2)
