@@ -141,6 +141,54 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
             "bound": "hbm", "timing": f"median of {steps} launches, HIP events"}
 
 
+def bench_scorer(wl, steps: int, warmup: int, seed: int = 0) -> dict:
+    """Retaining-head scorer (Sec. 3.4, App. B) on the same host share with
+    synthetic weights: bf16 GEMM [Lb x (n_q+2n_kv)d] x [. x 1024] fused with
+    SiLU and the per-KV-head output layer.  HIP events on the launch stream."""
+    import numpy as np
+    import torch
+    from paper_2502_12085_amd import apb, inputs
+
+    p = wl.problem
+    inp = inputs.make_inputs(wl, seed)
+    w = inputs.make_scorer_weights(p.n_q_heads, p.n_kv_heads, p.head_dim, seed=seed)
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    def f32(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    q, k, v, w1 = dev(inp["q"]), dev(inp["k"]), dev(inp["v"]), dev(w["w1"])
+    b1, w2, b2 = f32(w["b1"]), f32(w["w2"]), f32(w["b2"])
+    hidden = inputs.SCORER_HIDDEN
+    sp = apb.ScorerProblem(p.anchor_len, p.local_len, p.n_q_heads, p.n_kv_heads, p.head_dim, hidden)
+    ws = torch.empty(apb.scorer_workspace_size(sp), dtype=torch.uint8, device="cuda")
+    scores = torch.empty((p.n_kv_heads, p.local_len), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        apb.retaining_scores(sp, q, k, v, w1, b1, w2, b2, scores, ws, stream)
+    torch.cuda.synchronize()
+    t = []
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(steps):
+        e0.record(stream)
+        apb.retaining_scores(sp, q, k, v, w1, b1, w2, b2, scores, ws, stream)
+        e1.record(stream)
+        e1.synchronize()
+        t.append(e0.elapsed_time(e1))
+    us = 1e3 * sorted(t)[len(t) // 2]
+    feats = (p.n_q_heads + 2 * p.n_kv_heads) * p.head_dim
+    flops = 2.0 * p.local_len * feats * hidden + 2.0 * p.local_len * hidden * p.n_kv_heads
+    tf = flops / (us * 1e-6) / 1e12
+    return {"workload": wl.name, "local_len": p.local_len, "features": feats, "hidden": hidden,
+            "n_kv_heads": p.n_kv_heads, "us": round(us, 2), "flops": flops,
+            "tflops": round(tf, 1), "bound": "mfma", "peak": PEAK_BF16_TFLOPS,
+            "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+            "kernel": "scorer_gemm_kernel + scorer_reduce_kernel",
+            "timing": f"median of {steps} launches, HIP events", "weights": "synthetic"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,6 +201,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stage2", action="store_true",
                     help="skip the decoding-stage (Alg. 3) measurement")
+    ap.add_argument("--no-scorer", action="store_true",
+                    help="skip the retaining-head scorer measurement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (for scaling "
                          "the HBM byte counters) and exit")
@@ -270,6 +320,8 @@ def main():
                           "a800_implied_tflops": round(flops / 34.07e-3 / 1e12, 1),
                           "note": "8xA800 per-block breakdown at 128K; another machine"},
     }
+    if not args.no_scorer:
+        result["scorer"] = bench_scorer(wl, max(args.steps, 10), 3)
     if not args.no_stage2:
         result["stage2"] = [bench_stage2(inputs.DECODE_WORKLOADS[n], max(args.steps, 20), 5)
                             for n in ("llama8b_128k_decode", "llama8b_128k_question")]

@@ -11,12 +11,14 @@
  * over queries [A; B_h] and keys/values [A; P; B_h] under a modified mask
  * (Sec. 3.6, Eq. 2).
  *
- * This library exports the two kernels of that host share:
+ * This library exports the kernels of that host share:
  *   apb_compress_select  ArgTop-l_p of the local block's scores + gather of
  *                        the selected K/V rows (Sec. 3.4; Alg. 2, compression
  *                        step);
  *   apb_attention_fwd    the modified-mask attention (Eq. 2; Alg. 2,
  *                        attention step);
+ *   apb_retaining_scores the compressor's scores from a retaining head
+ *                        (Sec. 3.4) with caller-supplied weights;
  * and the decoding stage that follows the prefill (Alg. 3):
  *   apb_decode_attention one host's exact attention of the new tokens over
  *                        its KV cache, with the LSE;
@@ -45,7 +47,7 @@
 extern "C" {
 #endif
 
-#define APB_ABI_VERSION 2
+#define APB_ABI_VERSION 3
 
 typedef enum {
   APB_OK = 0,
@@ -124,6 +126,52 @@ apb_status_t apb_attention_fwd(const apb_problem_t* p, const uint16_t* q,
                                const uint16_t* k_pass, const uint16_t* v_pass,
                                uint16_t* o, float* lse, float softmax_scale,
                                void* stream);
+
+/* ------------------------------------------------------------------------
+ * Retaining-head scorer R (Sec. 3.4; Alg. 2, compression step; App. B): the
+ * importance of every local-block cache unit, the input of
+ * apb_compress_select.  The paper fixes only a small MLP over [Q, K, V] with
+ * intermediate size 1024; this library reads it as two linear layers with a
+ * SiLU between:
+ *   x_t = [Q_0[t] .. Q_{n_q-1}[t], K_0[t] .. K_{n_kv-1}[t], V_0[t] .. V_{n_kv-1}[t]]
+ *   scores[kv][t] = (W2 SiLU(W1 x_t + b1) + b2)[kv]
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t anchor_len; /* La >= 0: rows of Q/K/V before the local block      */
+  int32_t local_len;  /* Lb >= 1: local tokens to score                      */
+  int32_t n_q_heads;  /* n_q >= 1, a multiple of n_kv                        */
+  int32_t n_kv_heads; /* 1 <= n_kv <= 8 (one score per KV head)              */
+  int32_t head_dim;   /* d, in {64, 128}                                     */
+  int32_t hidden;     /* hidden units, a positive multiple of 256 (1024 in
+                         the paper)                                          */
+} apb_scorer_problem_t;
+
+/* Host-only checks of a scorer problem (no HIP call). */
+apb_status_t apb_validate_scorer(const apb_scorer_problem_t* p);
+
+/* Bytes of device workspace apb_retaining_scores needs (host only). */
+apb_status_t apb_scorer_workspace_size(const apb_scorer_problem_t* p, uint64_t* bytes);
+
+/*
+ * apb_retaining_scores -- the scores s_1..s_lb of Alg. 2 for one host.
+ *
+ *   q       bf16 [n_q][La+Lb][d]     k, v bf16 [n_kv][La+Lb][d]  (only rows
+ *                                    La.. are read)
+ *   w1      bf16 [hidden][(n_q + 2 n_kv) d]  first layer (out x in)
+ *   b1      fp32 [hidden]
+ *   w2      fp32 [n_kv][hidden]      second layer
+ *   b2      fp32 [n_kv]
+ *   scores  fp32 [n_kv][Lb]          the layout apb_compress_select takes
+ *   workspace, workspace_bytes  caller-owned device scratch of at least
+ *                   apb_scorer_workspace_size() bytes, 16-byte aligned.
+ * Arithmetic: bf16 products with fp32 accumulation for the first layer, fp32
+ * bias, SiLU and second layer; deterministic (fixed summation order).
+ */
+apb_status_t apb_retaining_scores(const apb_scorer_problem_t* p, const uint16_t* q,
+                                  const uint16_t* k, const uint16_t* v, const uint16_t* w1,
+                                  const float* b1, const float* w2, const float* b2,
+                                  float* scores, void* workspace, uint64_t workspace_bytes,
+                                  void* stream);
 
 /* ------------------------------------------------------------------------
  * Decoding stage (stage 2, Alg. 3).  Every host attends the new tokens'

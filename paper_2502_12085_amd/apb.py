@@ -20,7 +20,8 @@ STATUS_NAMES = {0: "APB_OK", 1: "APB_ERR_NULL_POINTER", 2: "APB_ERR_BAD_SHAPE",
 EXPORTED = ("apb_compress_select", "apb_attention_fwd", "apb_validate_problem",
             "apb_attention_flops", "apb_status_string", "apb_last_error", "apb_abi_version",
             "apb_validate_decode", "apb_decode_workspace_size", "apb_decode_attention",
-            "apb_merge_partials")
+            "apb_merge_partials", "apb_validate_scorer", "apb_scorer_workspace_size",
+            "apb_retaining_scores")
 
 
 class ApbError(RuntimeError):
@@ -60,6 +61,14 @@ class DecodeProblem(ctypes.Structure):
         return cls(*(int(getattr(p, f)) for f, _ in cls._fields_))
 
 
+class ScorerProblem(ctypes.Structure):
+    """``apb_scorer_problem_t``: one host's retaining-head scoring."""
+
+    _fields_ = [("anchor_len", ctypes.c_int32), ("local_len", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("hidden", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -97,6 +106,14 @@ def lib() -> ctypes.CDLL:
         L.apb_merge_partials.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp, vp,
                                          vp, vp, vp]
         L.apb_merge_partials.restype = ctypes.c_int
+        sp = ctypes.POINTER(ScorerProblem)
+        L.apb_validate_scorer.argtypes = [sp]
+        L.apb_validate_scorer.restype = ctypes.c_int
+        L.apb_scorer_workspace_size.argtypes = [sp, ctypes.POINTER(ctypes.c_uint64)]
+        L.apb_scorer_workspace_size.restype = ctypes.c_int
+        L.apb_retaining_scores.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_uint64,
+                                           vp]
+        L.apb_retaining_scores.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -213,3 +230,32 @@ def merge_partials(o_parts, lse_parts, o, lse=None, stream=None):
         _ptr(lse_parts, "lse_parts", f), _ptr(o, "o", _bf16_types()), _ptr(lse, "lse", f),
         _stream(stream))
     _check(st, "apb_merge_partials")
+
+
+def validate_scorer(problem) -> int:
+    return lib().apb_validate_scorer(ctypes.byref(problem))
+
+
+def scorer_workspace_size(problem) -> int:
+    """``apb_scorer_workspace_size``: device scratch bytes a scorer call needs."""
+    n = ctypes.c_uint64(0)
+    _check(lib().apb_scorer_workspace_size(ctypes.byref(problem), ctypes.byref(n)),
+           "apb_scorer_workspace_size")
+    return int(n.value)
+
+
+def retaining_scores(problem, q, k, v, w1, b1, w2, b2, scores, workspace, stream=None):
+    """``apb_retaining_scores``: retaining-head scores [n_kv, Lb] (fp32) of the
+    local rows of ``q``/``k``/``v`` with weights ``w1`` (bf16 [hidden, F]),
+    ``b1``, ``w2`` [n_kv, hidden], ``b2`` (fp32)."""
+    import torch
+    b = _bf16_types()
+    f = (torch.float32,)
+    if workspace is None or not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous device tensor")
+    st = lib().apb_retaining_scores(
+        ctypes.byref(problem), _ptr(q, "q", b), _ptr(k, "k", b), _ptr(v, "v", b),
+        _ptr(w1, "w1", b), _ptr(b1, "b1", f), _ptr(w2, "w2", f), _ptr(b2, "b2", f),
+        _ptr(scores, "scores", f), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "apb_retaining_scores")

@@ -164,6 +164,76 @@ apb_status_t apb_attention_fwd(const apb_problem_t* p, const uint16_t* q, const 
   return APB_OK;
 }
 
+apb_status_t apb_validate_scorer(const apb_scorer_problem_t* p) {
+  if (!p) return APB_ERR_NULL_POINTER;
+  if (p->anchor_len < 0 || p->local_len < 1) return APB_ERR_BAD_SHAPE;
+  if (p->n_kv_heads < 1 || p->n_q_heads < 1 || p->n_q_heads % p->n_kv_heads != 0)
+    return APB_ERR_BAD_SHAPE;
+  if (p->head_dim < 1 || p->hidden < 1) return APB_ERR_BAD_SHAPE;
+  if ((int64_t)p->anchor_len + p->local_len > kMaxRows) return APB_ERR_BAD_SHAPE;
+  if ((int64_t)(p->n_q_heads + 2 * p->n_kv_heads) * p->head_dim > (int64_t(1) << 20))
+    return APB_ERR_BAD_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 128) return APB_ERR_UNSUPPORTED;
+  if (p->n_kv_heads > apb::scorer_max_kv()) return APB_ERR_UNSUPPORTED;
+  if (p->hidden % apb::scorer_hidden_block() != 0) return APB_ERR_UNSUPPORTED;
+  return APB_OK;
+}
+
+static apb::ScorerArgs scorer_args(const apb_scorer_problem_t* p) {
+  apb::ScorerArgs a{};
+  a.La = p->anchor_len; a.Lb = p->local_len; a.n_q = p->n_q_heads; a.n_kv = p->n_kv_heads;
+  a.head_dim = p->head_dim; a.hidden = p->hidden;
+  return a;
+}
+
+apb_status_t apb_scorer_workspace_size(const apb_scorer_problem_t* p, uint64_t* bytes) {
+  const apb_status_t st = apb_validate_scorer(p);
+  if (st != APB_OK) return st;
+  if (!bytes) return APB_ERR_NULL_POINTER;
+  *bytes = apb::scorer_workspace_bytes(scorer_args(p));
+  return APB_OK;
+}
+
+apb_status_t apb_retaining_scores(const apb_scorer_problem_t* p, const uint16_t* q,
+                                  const uint16_t* k, const uint16_t* v, const uint16_t* w1,
+                                  const float* b1, const float* w2, const float* b2,
+                                  float* scores, void* workspace, uint64_t workspace_bytes,
+                                  void* stream) {
+  const apb_status_t st = apb_validate_scorer(p);
+  if (st != APB_OK) return st;
+  if (!q || !k || !v || !w1 || !b1 || !w2 || !b2 || !scores || !workspace)
+    return APB_ERR_NULL_POINTER;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(w1, 16) ||
+      !aligned(b1, 4) || !aligned(w2, 4) || !aligned(b2, 4) || !aligned(scores, 4) ||
+      !aligned(workspace, 16))
+    return APB_ERR_MISALIGNED;
+  apb::ScorerArgs a = scorer_args(p);
+  const uint64_t need = apb::scorer_workspace_bytes(a);
+  if (workspace_bytes < need) return APB_ERR_BAD_SHAPE;
+  const int64_t d = p->head_dim, M = (int64_t)p->anchor_len + p->local_len;
+  const int64_t F = (int64_t)(p->n_q_heads + 2 * p->n_kv_heads) * d;
+  const Range in[7] = {range_of(q, (int64_t)p->n_q_heads * M * d * 2),
+                       range_of(k, (int64_t)p->n_kv_heads * M * d * 2),
+                       range_of(v, (int64_t)p->n_kv_heads * M * d * 2),
+                       range_of(w1, (int64_t)p->hidden * F * 2), range_of(b1, (int64_t)p->hidden * 4),
+                       range_of(w2, (int64_t)p->n_kv_heads * p->hidden * 4),
+                       range_of(b2, (int64_t)p->n_kv_heads * 4)};
+  const Range out[2] = {range_of(scores, (int64_t)p->n_kv_heads * p->local_len * 4),
+                        range_of(workspace, (int64_t)need)};
+  for (const Range& r : out)
+    for (const Range& i : in)
+      if (overlaps(r, i)) return APB_ERR_ALIAS;
+  if (overlaps(out[0], out[1])) return APB_ERR_ALIAS;
+  a.q = q; a.k = k; a.v = v; a.w1 = w1; a.b1 = b1; a.w2 = w2; a.b2 = b2; a.scores = scores;
+  a.workspace = static_cast<float*>(workspace);
+  const hipError_t e = apb::launch_scorer(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    set_last_error(e);
+    return APB_ERR_HIP;
+  }
+  return APB_OK;
+}
+
 apb_status_t apb_validate_decode(const apb_decode_problem_t* p) {
   if (!p) return APB_ERR_NULL_POINTER;
   if (p->n_kv_heads < 1 || p->n_q_heads < 1 || p->n_q_heads % p->n_kv_heads != 0)

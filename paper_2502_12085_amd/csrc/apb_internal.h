@@ -1,5 +1,6 @@
 // Internal launch interface between the C-ABI layer (apb_api.hip) and the
-// gfx950 kernels (apb_attention.hip, apb_compress.hip, apb_decode.hip).
+// gfx950 kernels (apb_attention.hip, apb_compress.hip, apb_decode.hip,
+// apb_scorer.hip).
 // Not installed.
 #ifndef APB_INTERNAL_H_
 #define APB_INTERNAL_H_
@@ -67,11 +68,29 @@ struct MergeArgs {
   int32_t n_parts, rows, head_dim;
 };
 
+// Retaining-head scores of one host's local block, already validated.
+struct ScorerArgs {
+  const uint16_t* q;   // [n_q][La+Lb][d]
+  const uint16_t* k;   // [n_kv][La+Lb][d]
+  const uint16_t* v;
+  const uint16_t* w1;  // [hidden][(n_q + 2 n_kv) d] bf16
+  const float* b1;     // [hidden]
+  const float* w2;     // [n_kv][hidden]
+  const float* b2;     // [n_kv]
+  float* scores;       // [n_kv][Lb]
+  float* workspace;    // scorer_workspace_bytes()
+  int32_t La, Lb, n_q, n_kv, head_dim, hidden;
+};
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_compress(const CompressArgs& a, hipStream_t stream);
 DecodePlan plan_decode(const DecodeArgs& a);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
+uint64_t scorer_workspace_bytes(const ScorerArgs& a);
+hipError_t launch_scorer(const ScorerArgs& a, hipStream_t stream);
+int scorer_hidden_block();  // hidden must be a multiple of this
+int scorer_max_kv();        // largest n_kv the fused second layer takes
 
 }  // namespace apb
 

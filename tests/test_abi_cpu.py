@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(apb.EXPORTED)
     for name in declared:
         assert hasattr(L, name), name
-    assert apb.abi_version() == 2
+    assert apb.abi_version() == 3
 
 
 def _prob(**kw):
@@ -207,3 +207,55 @@ def test_merge_error_paths():
     assert L.apb_merge_partials(2, 4, 128, DO, DL, DQ + 2, WS, None) == 4
     assert L.apb_merge_partials(2, 4, 128, DO, DL, DO + 64, WS, None) == 6
     assert L.apb_merge_partials(2, 4, 128, DO, DL, DQ, DL + 4, None) == 6
+
+
+# ---------------------------------------------------- retaining-head scorer
+def _sprob(**kw):
+    base = dict(anchor_len=128, local_len=512, n_q_heads=4, n_kv_heads=1, head_dim=64, hidden=1024)
+    base.update(kw)
+    return apb.ScorerProblem(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), 0),
+    (dict(anchor_len=0), 0),
+    (dict(local_len=0), 2),
+    (dict(anchor_len=-1), 2),
+    (dict(n_q_heads=6, n_kv_heads=4), 2),
+    (dict(hidden=0), 2),
+    (dict(head_dim=96), 3),
+    (dict(n_q_heads=36, n_kv_heads=9), 3),   # more KV heads than the fused second layer takes
+    (dict(hidden=1000), 3),                  # not a multiple of 256
+])
+def test_validate_scorer(kw, code):
+    assert apb.validate_scorer(_sprob(**kw)) == code
+
+
+def test_scorer_workspace_size():
+    # one fp32 partial per 256 hidden units, KV head and local token
+    assert apb.scorer_workspace_size(_sprob()) == 4 * 1 * 512 * 4
+    assert apb.scorer_workspace_size(_sprob(n_q_heads=32, n_kv_heads=8, local_len=16384)) == 4 * 8 * 16384 * 4
+
+
+SQ_, SK_, SV_, SW1, SB1, SW2, SB2, SS, SWS = (A + i * (1 << 36) for i in range(9))
+
+
+def _score(p, q=SQ_, k=SK_, v=SV_, w1=SW1, b1=SB1, w2=SW2, b2=SB2, s=SS, ws=SWS, ws_bytes=1 << 30):
+    return apb.lib().apb_retaining_scores(ctypes.byref(p), q, k, v, w1, b1, w2, b2, s, ws,
+                                          ws_bytes, None)
+
+
+def test_scorer_error_paths():
+    p = _sprob()
+    assert _score(p, q=None) == 1
+    assert _score(p, w1=None) == 1
+    assert _score(p, b2=None) == 1
+    assert _score(p, ws=None) == 1
+    assert _score(p, ws_bytes=100) == 2
+    assert _score(p, w1=SW1 + 8) == 4
+    assert _score(p, b1=SB1 + 2) == 4
+    assert _score(p, ws=SWS + 4) == 4
+    assert _score(p, s=SQ_ + 64) == 6
+    assert _score(p, s=SW2) == 6
+    assert _score(p, ws=SS + 16) == 6
+    assert _score(_sprob(hidden=1000)) == 3
