@@ -80,6 +80,48 @@ def cpu_baseline(wl, inp, budget_s: float):
             "seconds": round(el, 3)}
 
 
+def busy_ahead(stream, ms: float = 20.0) -> None:
+    """Occupy the GPU with a spin kernel on `stream` while the host enqueues
+    the timed launches behind it, so that launches of a few microseconds run
+    back to back and their events do not include host submission gaps."""
+    import torch
+    torch.cuda.set_stream(stream)
+    torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
+
+
+def bench_mfma_ceiling(steps: int, seed: int = 0) -> dict:
+    """Matrix-core ceiling on this chip: the probe library's back-to-back
+    32x32x16 bf16 MFMA loop on random N(0,1) operands (one workgroup of 8
+    waves per CU, four independent accumulators per wave, no other work),
+    median of `steps` launches of about 2.5 ms each.  Under this load the
+    shader clock settles well below its 2.4 GHz peak, so the rate is the
+    ceiling a bf16 kernel can reach here, below the nominal peak."""
+    import torch
+    from paper_2502_12085_amd import probe
+
+    n_wg, iters = 256, 16384  # exactly one workgroup per CU, one round
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    ops = torch.randn(8192, generator=g).to(torch.bfloat16).cuda()
+    sink = torch.empty(n_wg * 512, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        probe.mfma_bf16(ops, sink, n_wg, iters, stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        probe.mfma_bf16(ops, sink, n_wg, iters, stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in ev)[len(ev) // 2]
+    tf = probe.mfma_flops(n_wg, iters) / (ms * 1e-3) / 1e12
+    return {"tflops": round(tf, 1), "frac_of_nominal_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+            "kernel": "mfma_loop_kernel (libapb_probe.so)",
+            "operands": "random N(0,1) bf16", "workgroups": n_wg, "waves_per_cu": 8,
+            "ms": round(ms, 3), "timing": f"median of {steps} launches, HIP events"}
+
+
 def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
     """Decoding stage (Alg. 3) at the same layer shape: the last host's
     partial attention over its cache plus the new tokens' K/V, and MergeScore
@@ -108,24 +150,27 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
     lse = torch.empty((rows,), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
 
-    def step():
+    def step(events=None):
+        if events:
+            events[0].record(stream)
         apb.decode_attention(prob, q, dkc, dvc, kn, vn, parts_o[H - 1].view(n_q, n_new, d),
                              parts_l[H - 1].view(n_q, n_new), ws, 0.0, stream)
-        e1.record(stream)
+        if events:
+            events[1].record(stream)
         apb.merge_partials(parts_o, parts_l, o, lse, stream)
+        if events:
+            events[2].record(stream)
 
-    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    t_dec, t_mrg = [], []
-    for _ in range(steps):
-        e0.record(stream)
-        step()
-        e2.record(stream)
-        e2.synchronize()
-        t_dec.append(e0.elapsed_time(e1))
-        t_mrg.append(e1.elapsed_time(e2))
+    busy_ahead(stream)
+    for e in ev:
+        step(e)
+    torch.cuda.synchronize()
+    t_dec = [a.elapsed_time(b) for a, b, _ in ev]
+    t_mrg = [b.elapsed_time(c) for _, b, c in ev]
     dec_us = 1e3 * sorted(t_dec)[len(t_dec) // 2]
     mrg_us = 1e3 * sorted(t_mrg)[len(t_mrg) // 2]
     keys = lc + n_new
@@ -138,7 +183,7 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
             "decode_hbm_frac": round(dec_bytes / (dec_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
             "merge_us": round(mrg_us, 2), "merge_algorithmic_bytes": mrg_bytes,
             "kernel": "decode_partial_kernel<128> + merge_kernel",
-            "bound": "hbm", "timing": f"median of {steps} launches, HIP events"}
+            "bound": "hbm", "timing": f"median of {steps} back-to-back launches, HIP events"}
 
 
 def bench_scorer(wl, steps: int, warmup: int, seed: int = 0) -> dict:
@@ -169,14 +214,15 @@ def bench_scorer(wl, steps: int, warmup: int, seed: int = 0) -> dict:
     for _ in range(warmup):
         apb.retaining_scores(sp, q, k, v, w1, b1, w2, b2, scores, ws, stream)
     torch.cuda.synchronize()
-    t = []
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for _ in range(steps):
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    busy_ahead(stream)
+    for e0, e1 in ev:
         e0.record(stream)
         apb.retaining_scores(sp, q, k, v, w1, b1, w2, b2, scores, ws, stream)
         e1.record(stream)
-        e1.synchronize()
-        t.append(e0.elapsed_time(e1))
+    torch.cuda.synchronize()
+    t = [a.elapsed_time(b) for a, b in ev]
     us = 1e3 * sorted(t)[len(t) // 2]
     feats = (p.n_q_heads + 2 * p.n_kv_heads) * p.head_dim
     flops = 2.0 * p.local_len * feats * hidden + 2.0 * p.local_len * hidden * p.n_kv_heads
@@ -186,7 +232,7 @@ def bench_scorer(wl, steps: int, warmup: int, seed: int = 0) -> dict:
             "tflops": round(tf, 1), "bound": "mfma", "peak": PEAK_BF16_TFLOPS,
             "frac": round(tf / PEAK_BF16_TFLOPS, 4),
             "kernel": "scorer_gemm_kernel + scorer_reduce_kernel",
-            "timing": f"median of {steps} launches, HIP events", "weights": "synthetic"}
+            "timing": f"median of {steps} back-to-back launches, HIP events", "weights": "synthetic"}
 
 
 def main():
@@ -203,6 +249,8 @@ def main():
                     help="skip the decoding-stage (Alg. 3) measurement")
     ap.add_argument("--no-scorer", action="store_true",
                     help="skip the retaining-head scorer measurement")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the matrix-core ceiling probe")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (for scaling "
                          "the HBM byte counters) and exit")
@@ -277,6 +325,20 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    # compressor with cold caches: a 1 GiB fill evicts L2 and the 256 MB
+    # Infinity Cache before each timed launch
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    cold = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(args.steps)]
+    for i, (c0, c1) in enumerate(cold):
+        flush.fill_(float(i))
+        c0.record(stream)
+        apb.compress_select(p, scores, k, v, idx, kbuf[p.host_idx], vbuf[p.host_idx], stream)
+        c1.record(stream)
+    torch.cuda.synchronize()
+    del flush
+    cold_us = 1e3 * sorted(a.elapsed_time(b) for a, b in cold)[len(cold) // 2]
+
     comp_ms = [a.elapsed_time(b) for a, b, _ in ev]
     attn_ms = [b.elapsed_time(c) for _, b, c in ev]
     ms_step = wall * 1e3 / args.steps
@@ -311,6 +373,8 @@ def main():
         "attention_ms": round(attn_avg, 4),
         "compress_us": round(1e3 * sum(comp_ms) / len(comp_ms), 2),
         "compress_gbs": round(comp_bytes / (sum(comp_ms) / len(comp_ms) * 1e-3) / 1e9, 1),
+        "compress_cold_us": round(cold_us, 2),
+        "compress_cold_gbs": round(comp_bytes / (cold_us * 1e-6) / 1e9, 1),
         "unmasked_flops": flops,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
@@ -320,6 +384,10 @@ def main():
                           "a800_implied_tflops": round(flops / 34.07e-3 / 1e12, 1),
                           "note": "8xA800 per-block breakdown at 128K; another machine"},
     }
+    if not args.no_ceiling:
+        ceil = bench_mfma_ceiling(max(args.steps // 2, 5))
+        ceil["attention_frac_of_ceiling"] = round(achieved / ceil["tflops"], 4)
+        result["mfma_ceiling"] = ceil
     if not args.no_scorer:
         result["scorer"] = bench_scorer(wl, max(args.steps, 10), 3)
     if not args.no_stage2:

@@ -1,4 +1,6 @@
-"""Build the gfx950 HIP library ``libapb.so`` in-tree with hipcc.
+"""Build the gfx950 HIP libraries in-tree with hipcc: ``libapb.so`` (the C
+ABI of ``include/apb.h``) and ``libapb_probe.so`` (the matrix-core ceiling
+probe of ``include/apb_probe.h``, used by the benchmark only).
 
 Usage: ``python -m paper_2502_12085_amd.build`` (or ``build()`` from
 Python).  Always recompiles.
@@ -14,6 +16,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libapb.so")
 SOURCES = ["apb_api.hip", "apb_attention.hip", "apb_compress.hip", "apb_decode.hip", "apb_scorer.hip"]
+PROBE_LIB = os.path.join(PKG, "libapb_probe.so")
+PROBE_SOURCES = ["probe_mfma.hip"]
 ARCH = "gfx950"
 
 
@@ -24,7 +28,8 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the APB library needs ROCm's hipcc")
 
 
-def compile_command(out: str = LIB) -> list:
+def compile_command(out: str = LIB, sources=None) -> list:
+    sources = SOURCES if sources is None else sources
     return [
         hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
         # packed fp32 VALU forms stay off: ordinary scalar fp32 code only
@@ -32,19 +37,24 @@ def compile_command(out: str = LIB) -> list:
         "-Wall", "-Wno-unused-function",
         "-I", os.path.join(ROOT, "include"),
         "-o", out,
-    ] + [os.path.join(CSRC, s) for s in SOURCES]
+    ] + [os.path.join(CSRC, src) for src in sources]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = compile_command(tmp)
+def _build_one(out: str, sources, verbose: bool) -> str:
+    tmp = out + ".tmp"
+    cmd = compile_command(tmp, sources)
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    _build_one(PROBE_LIB, PROBE_SOURCES, verbose)
+    return _build_one(LIB, SOURCES, verbose)
 
 
 if __name__ == "__main__":

@@ -259,3 +259,21 @@ def test_scorer_error_paths():
     assert _score(p, s=SW2) == 6
     assert _score(p, ws=SS + 16) == 6
     assert _score(_sprob(hidden=1000)) == 3
+
+
+def test_probe_library_exports_and_validates():
+    """libapb_probe.so exports what include/apb_probe.h declares and rejects
+    bad arguments on the host (fake addresses are never dereferenced)."""
+    from paper_2502_12085_amd import probe
+    text = open(os.path.join(ROOT, "include", "apb_probe.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    declared = sorted(set(re.findall(r"\b(apb_\w+)\s*\(", text)))
+    assert set(declared) == set(probe.EXPORTED)
+    L = probe.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+    assert probe.mfma_flops(256, 8) == 256 * 8 * 4 * 8 * 2 * 32 * 32 * 16
+    fake = 1 << 40
+    for args in [(None, fake, 1, 8), (fake, None, 1, 8), (fake, fake, 0, 8), (fake, fake, 1, 0),
+                 (fake, fake, 1, 12), (fake + 8, fake, 1, 8), (fake, fake, 1, (1 << 20) + 8)]:
+        assert L.apb_probe_mfma_bf16(*args, None) == 1, args
