@@ -51,16 +51,21 @@ def measured_traffic(workload: str):
     return t.get("hbm_bytes_per_launch")
 
 
+def _oracle_threads() -> int:
+    """Threads the oracle's BLAS calls use on this host."""
+    try:
+        from threadpoolctl import threadpool_info
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
+    except Exception:  # noqa: BLE001
+        return os.cpu_count() or 1
+
+
 def cpu_baseline(wl, inp, budget_s: float):
     """fp64 oracle on a bounded sample: whole query heads (all rows), as many
     as fit the time budget (at least one)."""
     import numpy as np
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # noqa: BLE001
-        cores = os.cpu_count() or 1
+    cores = _oracle_threads()
     p = wl.problem
     flops_head = oracle.attention_flops(1, p.head_dim, p.anchor_len, p.local_len, p.passing_rows)
     t0 = time.perf_counter()
@@ -122,7 +127,7 @@ def bench_mfma_ceiling(steps: int, seed: int = 0) -> dict:
             "ms": round(ms, 3), "timing": f"median of {steps} launches, HIP events"}
 
 
-def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
+def bench_stage2(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float = 0.0) -> dict:
     """Decoding stage (Alg. 3) at the same layer shape: the last host's
     partial attention over its cache plus the new tokens' K/V, and MergeScore
     of the H hosts' partials (the other hosts' partials are synthetic).  HIP
@@ -176,6 +181,20 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
     keys = lc + n_new
     dec_bytes = 2 * rows * d + 2 * 2 * n_kv * keys * d + 4 * rows * d + 4 * rows
     mrg_bytes = H * rows * (d + 1) * 4 + rows * d * 2 + rows * 4
+    cpu = None
+    if cpu_budget > 0:
+        import oracle
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            oracle.decode_attention_ref(case["q"], kc, vc, case["k_new"], case["v_new"])
+            reps += 1
+            if time.perf_counter() - t0 > cpu_budget or reps >= 20:
+                break
+        el = (time.perf_counter() - t0) / reps
+        cpu = {"value": round(dec_bytes / el / 1e9, 3), "unit": "GB/s", "us": round(el * 1e6, 1),
+               "cores": _oracle_threads(), "kind": "oracle",
+               "sample": f"the whole partial attention (fp64 NumPy), {reps} run(s)"}
     return {"workload": wl.name, "n_hosts": H, "cache_len": lc, "n_new": n_new,
             "n_q_heads": n_q, "n_kv_heads": n_kv, "head_dim": d,
             "decode_us": round(dec_us, 2), "decode_algorithmic_bytes": dec_bytes,
@@ -183,10 +202,11 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0) -> dict:
             "decode_hbm_frac": round(dec_bytes / (dec_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
             "merge_us": round(mrg_us, 2), "merge_algorithmic_bytes": mrg_bytes,
             "kernel": "decode_partial_kernel<128> + merge_kernel",
-            "bound": "hbm", "timing": f"median of {steps} back-to-back launches, HIP events"}
+            "bound": "hbm", "timing": f"median of {steps} back-to-back launches, HIP events",
+            "cpu_baseline": cpu}
 
 
-def bench_scorer(wl, steps: int, warmup: int, seed: int = 0) -> dict:
+def bench_scorer(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float = 0.0) -> dict:
     """Retaining-head scorer (Sec. 3.4, App. B) on the same host share with
     synthetic weights: bf16 GEMM [Lb x (n_q+2n_kv)d] x [. x 1024] fused with
     SiLU and the per-KV-head output layer.  HIP events on the launch stream."""
@@ -227,12 +247,30 @@ def bench_scorer(wl, steps: int, warmup: int, seed: int = 0) -> dict:
     feats = (p.n_q_heads + 2 * p.n_kv_heads) * p.head_dim
     flops = 2.0 * p.local_len * feats * hidden + 2.0 * p.local_len * hidden * p.n_kv_heads
     tf = flops / (us * 1e-6) / 1e12
+    cpu = None
+    if cpu_budget > 0:
+        import oracle
+        n_tok, el = 128, 0.0
+        while True:  # local tokens scored by the oracle: doubled until the budget is spent
+            rows = p.anchor_len + n_tok
+            t0 = time.perf_counter()
+            oracle.retaining_scores_ref(inp["q"][:, :rows], inp["k"][:, :rows], inp["v"][:, :rows],
+                                        w["w1"], w["b1"], w["w2"], w["b2"], anchor_len=p.anchor_len)
+            el = time.perf_counter() - t0
+            if el > cpu_budget / 3 or n_tok * 2 > p.local_len:
+                break
+            n_tok *= 2
+        f_s = 2.0 * n_tok * feats * hidden + 2.0 * n_tok * hidden * p.n_kv_heads
+        cpu = {"value": round(f_s / el / 1e12, 6), "unit": "TFLOP/s", "cores": _oracle_threads(),
+               "kind": "oracle", "sample": f"{n_tok} of {p.local_len} local tokens, fp64 NumPy; "
+                                           f"{el:.1f} s wall"}
     return {"workload": wl.name, "local_len": p.local_len, "features": feats, "hidden": hidden,
             "n_kv_heads": p.n_kv_heads, "us": round(us, 2), "flops": flops,
             "tflops": round(tf, 1), "bound": "mfma", "peak": PEAK_BF16_TFLOPS,
             "frac": round(tf / PEAK_BF16_TFLOPS, 4),
             "kernel": "scorer_gemm_kernel + scorer_reduce_kernel",
-            "timing": f"median of {steps} back-to-back launches, HIP events", "weights": "synthetic"}
+            "timing": f"median of {steps} back-to-back launches, HIP events", "weights": "synthetic",
+            "cpu_baseline": cpu}
 
 
 def main():
@@ -389,9 +427,11 @@ def main():
         ceil["attention_frac_of_ceiling"] = round(achieved / ceil["tflops"], 4)
         result["mfma_ceiling"] = ceil
     if not args.no_scorer:
-        result["scorer"] = bench_scorer(wl, max(args.steps, 10), 3)
+        result["scorer"] = bench_scorer(wl, max(args.steps, 10), 3,
+                                        cpu_budget=0.0 if args.no_cpu_baseline else 6.0)
     if not args.no_stage2:
-        result["stage2"] = [bench_stage2(inputs.DECODE_WORKLOADS[n], max(args.steps, 20), 5)
+        result["stage2"] = [bench_stage2(inputs.DECODE_WORKLOADS[n], max(args.steps, 20), 5,
+                                         cpu_budget=0.0 if args.no_cpu_baseline else 3.0)
                             for n in ("llama8b_128k_decode", "llama8b_128k_question")]
     if not args.no_cpu_baseline:
         print("# timing the fp64 oracle on the host cores", file=sys.stderr, flush=True)
