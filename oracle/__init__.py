@@ -27,3 +27,12 @@ from .scorer_oracle import (  # noqa: F401
     retaining_scores_ref,
     scorer_flops,
 )
+from .layer_oracle import (  # noqa: F401
+    rmsnorm_ref,
+    rope_ref,
+    swiglu_ffn_ref,
+    qkv_ref,
+    layer_ref,
+    layer_flops,
+    apb_table_flops_per_layer,
+)

@@ -259,3 +259,93 @@ def make_scorer_weights(n_q: int, n_kv: int, head_dim: int, hidden: int = SCORER
           * np.float32(1.0 / math.sqrt(hidden)))
     b2 = (r[3].standard_normal(n_kv, dtype=np.float32) * np.float32(0.1))
     return dict(w1=w1, b1=b1, w2=w2, b2=b2)
+
+
+# ------------------------------------------------------------ whole layer
+@dataclasses.dataclass(frozen=True)
+class LayerWorkload:
+    """One host's whole transformer layer around the host share (Alg. 2):
+    the attention problem plus the model's hidden size D, FFN intermediate
+    size I, the retaining head's hidden size, RMSNorm eps and RoPE base."""
+
+    name: str
+    attn: Workload
+    hidden: int
+    intermediate: int
+    scorer_hidden: int
+    eps: float = 1e-5
+    theta: float = 500000.0
+
+    @property
+    def problem(self) -> Problem:
+        return self.attn.problem
+
+
+# Llama-3.1-8B: D = 4096, I = 14336, 32/8 heads of 128; the tiny layer keeps
+# the tiny host share with D = n_q * d = 256.
+LAYER_WORKLOADS = {
+    "tiny_layer": LayerWorkload("tiny_layer", WORKLOADS["tiny"], 256, 512, 256),
+    "llama8b_32k_layer": LayerWorkload("llama8b_32k_layer", WORKLOADS["llama8b_32k"],
+                                       4096, 14336, SCORER_HIDDEN),
+    "llama8b_128k_layer": LayerWorkload("llama8b_128k_layer", WORKLOADS["llama8b_128k"],
+                                        4096, 14336, SCORER_HIDDEN),
+}
+
+
+def layer_positions(p: Problem) -> np.ndarray:
+    """Token positions of one host's rows (the RoPE input): anchor row r sits
+    at position r; local row i of host h at La + h*Lb + i, i.e. the local
+    blocks follow the anchor in document order."""
+    pos = np.empty(p.rows, np.int32)
+    pos[:p.anchor_len] = np.arange(p.anchor_len)
+    pos[p.anchor_len:] = p.anchor_len + p.host_idx * p.local_len + np.arange(p.local_len)
+    return pos
+
+
+def _normal_matrix_bf16(rng: np.random.Generator, rows: int, cols: int, std: float) -> np.ndarray:
+    out = np.empty((rows, cols), np.uint16)
+    step = max(1, (1 << 22) // max(cols, 1))
+    for r0 in range(0, rows, step):
+        r1 = min(rows, r0 + step)
+        out[r0:r1] = f32_to_bf16_bits(rng.standard_normal((r1 - r0, cols), dtype=np.float32)
+                                      * np.float32(std))
+    return out
+
+
+def make_layer_inputs(lw: LayerWorkload, seed: int = 0) -> dict:
+    """Inputs and synthetic weights of one host's layer.
+
+    Streams ``SeedSequence(seed + 3000).spawn(11)`` in the order hidden,
+    K_pass, V_pass, ln1, W_qkv, W_o, ln2, W_gate, W_up, W_down, (unused);
+    the retaining head from ``make_scorer_weights(..., seed=seed)``.
+    hidden [La+Lb, D] ~ N(0, 1); norm gains ~ 1 + N(0, 0.1^2); W_qkv, W_gate,
+    W_up ~ N(0, 1/D); W_o ~ N(0, 1/(n_q d)); W_down ~ N(0, 1/I); passing
+    K/V [host_idx, n_kv, l_p, d] ~ N(0, 1) (rows already rotated at their
+    source positions).  All bf16 bits except the retaining head's fp32
+    b1/w2/b2.  ``pos`` from ``layer_positions``."""
+    p = lw.problem
+    D, I = lw.hidden, lw.intermediate
+    nqkv = (p.n_q_heads + 2 * p.n_kv_heads) * p.head_dim
+    ss = np.random.SeedSequence(seed + 3000).spawn(11)
+    r = [np.random.default_rng(s) for s in ss]
+    hidden = _normal_matrix_bf16(r[0], p.rows, D, 1.0)
+    k_pass = np.empty((p.host_idx, p.n_kv_heads, p.pass_len, p.head_dim), np.uint16)
+    v_pass = np.empty_like(k_pass)
+    for s in range(p.host_idx):
+        k_pass[s] = _normal_bf16(r[1], k_pass.shape[1:])
+        v_pass[s] = _normal_bf16(r[2], v_pass.shape[1:])
+    gain = lambda rng: f32_to_bf16_bits(np.float32(1.0) + rng.standard_normal(D, dtype=np.float32)  # noqa: E731
+                                        * np.float32(0.1))
+    w = dict(
+        ln1=gain(r[3]),
+        w_qkv=_normal_matrix_bf16(r[4], nqkv, D, 1.0 / math.sqrt(D)),
+        w_o=_normal_matrix_bf16(r[5], D, p.n_q_heads * p.head_dim,
+                                1.0 / math.sqrt(p.n_q_heads * p.head_dim)),
+        ln2=gain(r[6]),
+        w_gate=_normal_matrix_bf16(r[7], I, D, 1.0 / math.sqrt(D)),
+        w_up=_normal_matrix_bf16(r[8], I, D, 1.0 / math.sqrt(D)),
+        w_down=_normal_matrix_bf16(r[9], D, I, 1.0 / math.sqrt(I)),
+    )
+    w.update(make_scorer_weights(p.n_q_heads, p.n_kv_heads, p.head_dim, lw.scorer_hidden,
+                                 seed=seed))
+    return dict(hidden=hidden, pos=layer_positions(p), k_pass=k_pass, v_pass=v_pass, w=w)
