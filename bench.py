@@ -127,6 +127,64 @@ def bench_mfma_ceiling(steps: int, seed: int = 0) -> dict:
             "ms": round(ms, 3), "timing": f"median of {steps} launches, HIP events"}
 
 
+def bench_layer(lw, steps: int, warmup: int, seed: int = 0) -> dict:
+    """One host's whole layer (Alg. 2 with the model's layer around the host
+    share): apb_layer_fwd on synthetic weights, inputs resident in HBM, HIP
+    events around each call on the launch stream."""
+    import numpy as np
+    import torch
+    from paper_2502_12085_amd import apb, inputs
+
+    p = lw.problem
+    inp = inputs.make_layer_inputs(lw, seed)
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    w = {k: dev(inp["w"][v]) for k, v in (("ln1", "ln1"), ("w_qkv", "w_qkv"), ("w_o", "w_o"),
+                                         ("ln2", "ln2"), ("w_gate", "w_gate"), ("w_up", "w_up"),
+                                         ("w_down", "w_down"), ("r_w1", "w1"))}
+    for k, v in (("r_b1", "b1"), ("r_w2", "w2"), ("r_b2", "b2")):
+        w[k] = torch.from_numpy(np.ascontiguousarray(inp["w"][v])).cuda()
+    hidden, pos = dev(inp["hidden"]), torch.from_numpy(inp["pos"]).cuda()
+    pk = torch.zeros((p.n_hosts, p.n_kv_heads, p.pass_len, p.head_dim), dtype=torch.bfloat16,
+                     device="cuda")
+    pv = torch.zeros_like(pk)
+    pk[:p.host_idx] = dev(inp["k_pass"])
+    pv[:p.host_idx] = dev(inp["v_pass"])
+    kc = torch.empty((p.n_kv_heads, p.rows, p.head_dim), dtype=torch.bfloat16, device="cuda")
+    vc = torch.empty_like(kc)
+    out = torch.empty((p.rows, lw.hidden), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(apb.layer_workspace_size(lw), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def call():
+        apb.layer_fwd(lw, w, hidden, pos, kc, vc, pk, pv, out, ws, stream)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        call()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in ev)[len(ev) // 2]
+    flops = apb.layer_flops(lw)
+    return {"workload": lw.name, "hidden": lw.hidden, "intermediate": lw.intermediate,
+            "rows": p.rows, "ms": round(ms, 3), "flops": flops,
+            "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+            "frac_of_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "kernels": "rmsnorm, gemm(QKV), rope, scorer, compressor, attention, gemm(O), "
+                       "rmsnorm, gemm(gate/up + SwiGLU), gemm(down)",
+            "timing": f"median of {steps} calls, HIP events", "weights": "synthetic",
+            "paper_context": {"a800_block_ms": 80.18,
+                              "note": "8xA800 per-block wall time at 128K (the paper's "
+                                      "block breakdown); another machine"}}
+
+
 def bench_stage2(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float = 0.0) -> dict:
     """Decoding stage (Alg. 3) at the same layer shape: the last host's
     partial attention over its cache plus the new tokens' K/V, and MergeScore
@@ -287,6 +345,8 @@ def main():
                     help="skip the decoding-stage (Alg. 3) measurement")
     ap.add_argument("--no-scorer", action="store_true",
                     help="skip the retaining-head scorer measurement")
+    ap.add_argument("--no-layer", action="store_true",
+                    help="skip the whole-layer (Alg. 2) measurement")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the matrix-core ceiling probe")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -426,6 +486,10 @@ def main():
         ceil = bench_mfma_ceiling(max(args.steps // 2, 5))
         ceil["attention_frac_of_ceiling"] = round(achieved / ceil["tflops"], 4)
         result["mfma_ceiling"] = ceil
+    if not args.no_layer and args.workload in ("llama8b_128k", "llama8b_32k"):
+        print("# whole-layer measurement", file=sys.stderr, flush=True)
+        result["layer"] = bench_layer(inputs.LAYER_WORKLOADS[args.workload + "_layer"],
+                                      max(args.steps // 2, 5), 2)
     if not args.no_scorer:
         result["scorer"] = bench_scorer(wl, max(args.steps, 10), 3,
                                         cpu_budget=0.0 if args.no_cpu_baseline else 6.0)

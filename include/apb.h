@@ -19,6 +19,8 @@
  *                        attention step);
  *   apb_retaining_scores the compressor's scores from a retaining head
  *                        (Sec. 3.4) with caller-supplied weights;
+ *   apb_layer_fwd        the whole layer of one host around these kernels
+ *                        (Alg. 2: projections, norms, RoPE, FFN);
  * and the decoding stage that follows the prefill (Alg. 3):
  *   apb_decode_attention one host's exact attention of the new tokens over
  *                        its KV cache, with the LSE;
@@ -47,7 +49,7 @@
 extern "C" {
 #endif
 
-#define APB_ABI_VERSION 3
+#define APB_ABI_VERSION 4
 
 typedef enum {
   APB_OK = 0,
@@ -240,6 +242,85 @@ apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t*
 apb_status_t apb_merge_partials(int32_t n_parts, int32_t rows, int32_t head_dim,
                                 const float* o_parts, const float* lse_parts, uint16_t* o,
                                 float* lse, void* stream);
+
+/* ------------------------------------------------------------------------
+ * One host's whole layer (Alg. 2): the QKV projection of the anchor and
+ * local hidden states, the retaining head R over the local block, ArgTop-l_p
+ * and gather into this host's passing slot, attention over [A; P; B] with
+ * the earlier hosts' slots, and the FFN.  The layer around attention is the
+ * model's own; the paper does not restate it, and this library reads it as a
+ * Llama-style pre-norm block:
+ *   x = RMSNorm(H; ln1);  Q, K, V = heads of x W_qkv^T;  Q, K = RoPE(Q, K, pos)
+ *   scores = R([Q_B, K_B, V_B]);  slot host_idx = K_B, V_B rows ArgTop-l_p
+ *   A = apb_attention_fwd(Q, K, V, slots 0..host_idx-1)
+ *   H1 = H + concat_heads(A) W_o^T;  y = RMSNorm(H1; ln2)
+ *   out = H1 + (SiLU(y W_gate^T) * (y W_up^T)) W_down^T
+ * RMSNorm(h)_c = h_c / sqrt(mean(h^2) + eps) * ln_c.  RoPE rotates the pair
+ * (j, j + d/2) of every Q and K head by pos[t] * theta^(-2j/d).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  apb_problem_t attn;     /* the host share (H, host_idx, La, Lb, l_p, heads) */
+  int32_t hidden;         /* D >= 64, a multiple of 64                       */
+  int32_t intermediate;   /* I >= 64, a multiple of 64 (FFN)                 */
+  int32_t scorer_hidden;  /* retaining head's hidden units, as for
+                             apb_retaining_scores (1024 in the paper)         */
+  float rms_eps;          /* > 0                                             */
+  float rope_theta;       /* > 1                                             */
+} apb_layer_problem_t;
+
+/* Weights of one layer, all caller-owned device memory, bf16 row-major
+ * (rows = outputs) unless noted. */
+typedef struct {
+  const uint16_t* ln1;     /* [D]                                            */
+  const uint16_t* w_qkv;   /* [(n_q + 2 n_kv) d][D]: Q heads, K heads, V heads */
+  const uint16_t* w_o;     /* [D][n_q d]                                     */
+  const uint16_t* ln2;     /* [D]                                            */
+  const uint16_t* w_gate;  /* [I][D]                                         */
+  const uint16_t* w_up;    /* [I][D]                                         */
+  const uint16_t* w_down;  /* [D][I]                                         */
+  const uint16_t* r_w1;    /* retaining head W1 bf16 [hidden_r][(n_q + 2 n_kv) d] */
+  const float* r_b1;       /* fp32 [hidden_r]                                */
+  const float* r_w2;       /* fp32 [n_kv][hidden_r]                          */
+  const float* r_b2;       /* fp32 [n_kv]                                    */
+} apb_layer_weights_t;
+
+/* Host-only checks of a layer problem (no HIP call): the host share as in
+ * apb_validate_problem, the retaining head as in apb_validate_scorer, D and
+ * I multiples of 64, eps > 0, theta > 1. */
+apb_status_t apb_validate_layer(const apb_layer_problem_t* p);
+
+/* Bytes of device workspace apb_layer_fwd needs (host only). */
+apb_status_t apb_layer_workspace_size(const apb_layer_problem_t* p, uint64_t* bytes);
+
+/* Matrix-product FLOPs of one apb_layer_fwd call: the QKV, O and three FFN
+ * products (2 flops per multiply-add), the retaining head's two layers and
+ * the unmasked attention (apb_attention_flops).  Host-only; -1 if invalid. */
+double apb_layer_flops(const apb_layer_problem_t* p);
+
+/*
+ * apb_layer_fwd -- one host's layer (Alg. 2).  T = La + Lb rows.
+ *
+ *   w           weights (above); every pointer required.
+ *   hidden_in   bf16 [T][D]    anchor rows then local rows.
+ *   positions   int32 [T]      RoPE position of every row.
+ *   k_cache, v_cache  bf16 [n_kv][T][d]  out: the layer's KV cache (Alg. 2
+ *                              returns it), K after RoPE.
+ *   pass_k, pass_v    bf16 [H][n_kv][l_p][d] rank-major passing buffer:
+ *                              slots 0..host_idx-1 are read (the earlier
+ *                              hosts' blocks, already rotated), slot
+ *                              host_idx is written (this host's block).
+ *                              May be NULL only when l_p == 0.
+ *   hidden_out  bf16 [T][D]    out.
+ *   workspace   >= apb_layer_workspace_size() bytes, 16-byte aligned.
+ * Arithmetic: bf16 operands and intermediates (x, Q/K/V, A, H1, y and the
+ * SwiGLU product are stored in bf16), fp32 accumulation, norms, RoPE angles
+ * in fp64 with fp32 rotation, residual sums in fp32 before rounding.
+ */
+apb_status_t apb_layer_fwd(const apb_layer_problem_t* p, const apb_layer_weights_t* w,
+                           const uint16_t* hidden_in, const int32_t* positions,
+                           uint16_t* k_cache, uint16_t* v_cache, uint16_t* pass_k,
+                           uint16_t* pass_v, uint16_t* hidden_out, void* workspace,
+                           uint64_t workspace_bytes, void* stream);
 
 /* Host-only checks of a problem description (no HIP call). */
 apb_status_t apb_validate_problem(const apb_problem_t* p);

@@ -21,7 +21,8 @@ EXPORTED = ("apb_compress_select", "apb_attention_fwd", "apb_validate_problem",
             "apb_attention_flops", "apb_status_string", "apb_last_error", "apb_abi_version",
             "apb_validate_decode", "apb_decode_workspace_size", "apb_decode_attention",
             "apb_merge_partials", "apb_validate_scorer", "apb_scorer_workspace_size",
-            "apb_retaining_scores")
+            "apb_retaining_scores", "apb_validate_layer", "apb_layer_workspace_size",
+            "apb_layer_flops", "apb_layer_fwd")
 
 
 class ApbError(RuntimeError):
@@ -69,6 +70,30 @@ class ScorerProblem(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("hidden", ctypes.c_int32)]
 
 
+class LayerProblem(ctypes.Structure):
+    """``apb_layer_problem_t``: one host's whole layer (Alg. 2)."""
+
+    _fields_ = [("attn", Problem), ("hidden", ctypes.c_int32), ("intermediate", ctypes.c_int32),
+                ("scorer_hidden", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_theta", ctypes.c_float)]
+
+    @classmethod
+    def of(cls, lw) -> "LayerProblem":
+        """From an object with ``problem``, ``hidden``, ``intermediate``,
+        ``scorer_hidden``, ``eps`` and ``theta`` (e.g. inputs.LayerWorkload)."""
+        if isinstance(lw, cls):
+            return lw
+        return cls(Problem.of(lw.problem), int(lw.hidden), int(lw.intermediate),
+                   int(lw.scorer_hidden), float(lw.eps), float(lw.theta))
+
+
+class LayerWeights(ctypes.Structure):
+    """``apb_layer_weights_t``: device pointers of one layer's weights."""
+
+    _fields_ = [(n, ctypes.c_void_p) for n in ("ln1", "w_qkv", "w_o", "ln2", "w_gate", "w_up",
+                                               "w_down", "r_w1", "r_b1", "r_w2", "r_b2")]
+
+
 _lib = None
 
 
@@ -114,6 +139,16 @@ def lib() -> ctypes.CDLL:
         L.apb_retaining_scores.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_uint64,
                                            vp]
         L.apb_retaining_scores.restype = ctypes.c_int
+        lp_ = ctypes.POINTER(LayerProblem)
+        L.apb_validate_layer.argtypes = [lp_]
+        L.apb_validate_layer.restype = ctypes.c_int
+        L.apb_layer_workspace_size.argtypes = [lp_, ctypes.POINTER(ctypes.c_uint64)]
+        L.apb_layer_workspace_size.restype = ctypes.c_int
+        L.apb_layer_flops.argtypes = [lp_]
+        L.apb_layer_flops.restype = ctypes.c_double
+        L.apb_layer_fwd.argtypes = [lp_, ctypes.POINTER(LayerWeights), vp, vp, vp, vp, vp, vp, vp,
+                                    vp, ctypes.c_uint64, vp]
+        L.apb_layer_fwd.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -259,3 +294,43 @@ def retaining_scores(problem, q, k, v, w1, b1, w2, b2, scores, workspace, stream
         _ptr(scores, "scores", f), workspace.data_ptr(),
         workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "apb_retaining_scores")
+
+
+def validate_layer(problem) -> int:
+    return lib().apb_validate_layer(ctypes.byref(LayerProblem.of(problem)))
+
+
+def layer_workspace_size(problem) -> int:
+    """``apb_layer_workspace_size``: device scratch bytes a layer call needs."""
+    n = ctypes.c_uint64(0)
+    _check(lib().apb_layer_workspace_size(ctypes.byref(LayerProblem.of(problem)), ctypes.byref(n)),
+           "apb_layer_workspace_size")
+    return int(n.value)
+
+
+def layer_flops(problem) -> float:
+    return lib().apb_layer_flops(ctypes.byref(LayerProblem.of(problem)))
+
+
+def layer_fwd(problem, weights: dict, hidden_in, positions, k_cache, v_cache, pass_k, pass_v,
+              hidden_out, workspace, stream=None):
+    """``apb_layer_fwd``: one host's whole layer (Alg. 2).  ``weights`` maps the
+    ``apb_layer_weights_t`` field names to device tensors (bf16, the
+    retaining head's r_b1/r_w2/r_b2 fp32); ``pass_k``/``pass_v`` are the
+    rank-major [H, n_kv, l_p, d] passing buffers (slots < host_idx read, slot
+    host_idx written)."""
+    import torch
+    b = _bf16_types()
+    f = (torch.float32,)
+    w = LayerWeights()
+    for name, _ in LayerWeights._fields_:
+        setattr(w, name, _ptr(weights[name], name, f if name in ("r_b1", "r_w2", "r_b2") else b))
+    if workspace is None or not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous device tensor")
+    st = lib().apb_layer_fwd(
+        ctypes.byref(LayerProblem.of(problem)), ctypes.byref(w), _ptr(hidden_in, "hidden_in", b),
+        _ptr(positions, "positions", (torch.int32,)), _ptr(k_cache, "k_cache", b),
+        _ptr(v_cache, "v_cache", b), _ptr(pass_k, "pass_k", b), _ptr(pass_v, "pass_v", b),
+        _ptr(hidden_out, "hidden_out", b), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "apb_layer_fwd")

@@ -15,7 +15,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libapb.so")
-SOURCES = ["apb_api.hip", "apb_attention.hip", "apb_compress.hip", "apb_decode.hip", "apb_scorer.hip"]
+SOURCES = ["apb_api.hip", "apb_attention.hip", "apb_compress.hip", "apb_decode.hip", "apb_scorer.hip",
+           "apb_layer.hip"]
 PROBE_LIB = os.path.join(PKG, "libapb_probe.so")
 PROBE_SOURCES = ["probe_mfma.hip"]
 ARCH = "gfx950"

@@ -234,6 +234,120 @@ apb_status_t apb_retaining_scores(const apb_scorer_problem_t* p, const uint16_t*
   return APB_OK;
 }
 
+static apb_scorer_problem_t layer_scorer_problem(const apb_layer_problem_t* p) {
+  apb_scorer_problem_t s;
+  s.anchor_len = p->attn.anchor_len; s.local_len = p->attn.local_len;
+  s.n_q_heads = p->attn.n_q_heads; s.n_kv_heads = p->attn.n_kv_heads;
+  s.head_dim = p->attn.head_dim; s.hidden = p->scorer_hidden;
+  return s;
+}
+
+apb_status_t apb_validate_layer(const apb_layer_problem_t* p) {
+  if (!p) return APB_ERR_NULL_POINTER;
+  apb_status_t st = apb_validate_problem(&p->attn);
+  if (st != APB_OK) return st;
+  const apb_scorer_problem_t sp = layer_scorer_problem(p);
+  st = apb_validate_scorer(&sp);
+  if (st != APB_OK) return st;
+  if (p->hidden < 64 || p->hidden % 64 != 0 || p->intermediate < 64 || p->intermediate % 64 != 0)
+    return APB_ERR_BAD_SHAPE;
+  if (p->hidden > (1 << 20) || p->intermediate > (1 << 20)) return APB_ERR_BAD_SHAPE;
+  if (!(p->rms_eps > 0.f) || !isfinite(p->rms_eps) || !(p->rope_theta > 1.f) ||
+      !isfinite(p->rope_theta))
+    return APB_ERR_BAD_SHAPE;
+  return APB_OK;
+}
+
+static apb::LayerArgs layer_args(const apb_layer_problem_t* p) {
+  apb::LayerArgs a{};
+  a.host_idx = p->attn.host_idx; a.La = p->attn.anchor_len; a.Lb = p->attn.local_len;
+  a.lp = p->attn.pass_len; a.n_q = p->attn.n_q_heads; a.n_kv = p->attn.n_kv_heads;
+  a.head_dim = p->attn.head_dim; a.D = p->hidden; a.I = p->intermediate;
+  a.scorer_hidden = p->scorer_hidden; a.eps = p->rms_eps; a.theta = p->rope_theta;
+  return a;
+}
+
+apb_status_t apb_layer_workspace_size(const apb_layer_problem_t* p, uint64_t* bytes) {
+  const apb_status_t st = apb_validate_layer(p);
+  if (st != APB_OK) return st;
+  if (!bytes) return APB_ERR_NULL_POINTER;
+  *bytes = apb::layer_workspace_bytes(layer_args(p));
+  return APB_OK;
+}
+
+double apb_layer_flops(const apb_layer_problem_t* p) {
+  if (apb_validate_layer(p) != APB_OK) return -1.0;
+  const double T = (double)p->attn.anchor_len + p->attn.local_len;
+  const double D = p->hidden, I = p->intermediate, d = p->attn.head_dim;
+  const double nq = p->attn.n_q_heads, nkv = p->attn.n_kv_heads;
+  const double Fr = (nq + 2 * nkv) * d, hr = p->scorer_hidden, Lb = p->attn.local_len;
+  return 2 * T * D * (nq + 2 * nkv) * d + 2 * T * nq * d * D + 6 * T * D * I +
+         2 * Lb * Fr * hr + 2 * Lb * hr * nkv + apb_attention_flops(&p->attn);
+}
+
+apb_status_t apb_layer_fwd(const apb_layer_problem_t* p, const apb_layer_weights_t* w,
+                           const uint16_t* hidden_in, const int32_t* positions,
+                           uint16_t* k_cache, uint16_t* v_cache, uint16_t* pass_k,
+                           uint16_t* pass_v, uint16_t* hidden_out, void* workspace,
+                           uint64_t workspace_bytes, void* stream) {
+  const apb_status_t st = apb_validate_layer(p);
+  if (st != APB_OK) return st;
+  if (!w || !hidden_in || !positions || !k_cache || !v_cache || !hidden_out || !workspace)
+    return APB_ERR_NULL_POINTER;
+  if (!w->ln1 || !w->w_qkv || !w->w_o || !w->ln2 || !w->w_gate || !w->w_up || !w->w_down ||
+      !w->r_w1 || !w->r_b1 || !w->r_w2 || !w->r_b2)
+    return APB_ERR_NULL_POINTER;
+  const apb_problem_t& ap = p->attn;
+  if (ap.pass_len > 0 && (!pass_k || !pass_v)) return APB_ERR_NULL_POINTER;
+  const void* b16[] = {w->ln1, w->w_qkv, w->w_o, w->ln2, w->w_gate, w->w_up, w->w_down, w->r_w1,
+                       hidden_in, k_cache, v_cache, hidden_out, workspace};
+  for (const void* ptr : b16)
+    if (!aligned(ptr, 16)) return APB_ERR_MISALIGNED;
+  if (!aligned(w->r_b1, 4) || !aligned(w->r_w2, 4) || !aligned(w->r_b2, 4) ||
+      !aligned(positions, 4))
+    return APB_ERR_MISALIGNED;
+  if (ap.pass_len > 0 && (!aligned(pass_k, 16) || !aligned(pass_v, 16))) return APB_ERR_MISALIGNED;
+  apb::LayerArgs a = layer_args(p);
+  const uint64_t need = apb::layer_workspace_bytes(a);
+  if (workspace_bytes < need) return APB_ERR_BAD_SHAPE;
+
+  const int64_t T = (int64_t)ap.anchor_len + ap.local_len, D = p->hidden, I = p->intermediate;
+  const int64_t d = ap.head_dim, nq = ap.n_q_heads, nkv = ap.n_kv_heads;
+  const int64_t Fr = (nq + 2 * nkv) * d, hr = p->scorer_hidden;
+  const int64_t slot = nkv * (int64_t)ap.pass_len * d * 2;  // bytes of one passing slot
+  const bool pass = ap.pass_len > 0;
+  const Range in[15] = {
+      range_of(hidden_in, T * D * 2), range_of(positions, T * 4), range_of(w->ln1, D * 2),
+      range_of(w->w_qkv, Fr * D * 2), range_of(w->w_o, D * nq * d * 2), range_of(w->ln2, D * 2),
+      range_of(w->w_gate, I * D * 2), range_of(w->w_up, I * D * 2), range_of(w->w_down, D * I * 2),
+      range_of(w->r_w1, hr * Fr * 2), range_of(w->r_b1, hr * 4), range_of(w->r_w2, nkv * hr * 4),
+      range_of(w->r_b2, nkv * 4), range_of(pass ? pass_k : nullptr, ap.host_idx * slot),
+      range_of(pass ? pass_v : nullptr, ap.host_idx * slot)};
+  const Range out[6] = {range_of(k_cache, nkv * T * d * 2), range_of(v_cache, nkv * T * d * 2),
+                        range_of(hidden_out, T * D * 2), range_of(workspace, (int64_t)need),
+                        range_of(pass ? (const uint8_t*)pass_k + ap.host_idx * slot : nullptr, slot),
+                        range_of(pass ? (const uint8_t*)pass_v + ap.host_idx * slot : nullptr, slot)};
+  for (const Range& r : out)
+    for (const Range& i : in)
+      if (overlaps(r, i)) return APB_ERR_ALIAS;
+  for (int i = 0; i < 6; ++i)
+    for (int j = i + 1; j < 6; ++j)
+      if (overlaps(out[i], out[j])) return APB_ERR_ALIAS;
+
+  a.hidden = hidden_in; a.pos = positions;
+  a.ln1 = w->ln1; a.w_qkv = w->w_qkv; a.w_o = w->w_o; a.ln2 = w->ln2; a.w_gate = w->w_gate;
+  a.w_up = w->w_up; a.w_down = w->w_down; a.r_w1 = w->r_w1; a.r_b1 = w->r_b1; a.r_w2 = w->r_w2;
+  a.r_b2 = w->r_b2; a.k_cache = k_cache; a.v_cache = v_cache;
+  a.pass_k = pass ? pass_k : nullptr; a.pass_v = pass ? pass_v : nullptr;
+  a.hidden_out = hidden_out; a.workspace = workspace;
+  const hipError_t e = apb::launch_layer(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    set_last_error(e);
+    return APB_ERR_HIP;
+  }
+  return APB_OK;
+}
+
 apb_status_t apb_validate_decode(const apb_decode_problem_t* p) {
   if (!p) return APB_ERR_NULL_POINTER;
   if (p->n_kv_heads < 1 || p->n_q_heads < 1 || p->n_q_heads % p->n_kv_heads != 0)

@@ -1,6 +1,6 @@
 // Internal launch interface between the C-ABI layer (apb_api.hip) and the
 // gfx950 kernels (apb_attention.hip, apb_compress.hip, apb_decode.hip,
-// apb_scorer.hip).
+// apb_scorer.hip, apb_layer.hip).
 // Not installed.
 #ifndef APB_INTERNAL_H_
 #define APB_INTERNAL_H_
@@ -82,6 +82,32 @@ struct ScorerArgs {
   int32_t La, Lb, n_q, n_kv, head_dim, hidden;
 };
 
+// One host's whole layer (Alg. 2 with the model's layer), already validated.
+struct LayerArgs {
+  const uint16_t* hidden;    // [T][D], T = La + Lb
+  const int32_t* pos;        // [T]
+  const uint16_t* ln1;       // [D]
+  const uint16_t* w_qkv;     // [(n_q + 2 n_kv) d][D]
+  const uint16_t* w_o;       // [D][n_q d]
+  const uint16_t* ln2;       // [D]
+  const uint16_t* w_gate;    // [I][D]
+  const uint16_t* w_up;      // [I][D]
+  const uint16_t* w_down;    // [D][I]
+  const uint16_t* r_w1;      // retaining head, as ScorerArgs
+  const float* r_b1;
+  const float* r_w2;
+  const float* r_b2;
+  uint16_t* k_cache;         // out [n_kv][T][d] (post-RoPE)
+  uint16_t* v_cache;         // out [n_kv][T][d]
+  uint16_t* pass_k;          // [H][n_kv][lp][d]: slots < host_idx read, slot host_idx written
+  uint16_t* pass_v;
+  uint16_t* hidden_out;      // out [T][D]
+  void* workspace;           // layer_workspace_bytes()
+  int32_t host_idx, La, Lb, lp;
+  int32_t n_q, n_kv, head_dim, D, I, scorer_hidden;
+  float eps, theta;
+};
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_compress(const CompressArgs& a, hipStream_t stream);
 DecodePlan plan_decode(const DecodeArgs& a);
@@ -91,6 +117,8 @@ uint64_t scorer_workspace_bytes(const ScorerArgs& a);
 hipError_t launch_scorer(const ScorerArgs& a, hipStream_t stream);
 int scorer_hidden_block();  // hidden must be a multiple of this
 int scorer_max_kv();        // largest n_kv the fused second layer takes
+uint64_t layer_workspace_bytes(const LayerArgs& a);
+hipError_t launch_layer(const LayerArgs& a, hipStream_t stream);
 
 }  // namespace apb
 

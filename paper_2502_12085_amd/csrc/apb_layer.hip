@@ -1,0 +1,416 @@
+// One host's whole APB layer (Alg. 2 with the model's layer around the
+// attention) for gfx950: RMSNorm, the QKV projection, RoPE, the retaining
+// head, top-l_p selection and gather, the modified-mask attention, the O
+// projection with its residual, RMSNorm, and the SwiGLU FFN with its
+// residual.  The retaining head, the compressor and the attention are the
+// library's own kernels; this file adds the layer's norms, rotary embedding
+// and matrix products, and sequences the whole layer on one stream.
+//
+// Matrix products.  Every projection is out[t][f] = sum_k x[t][k] W[f][k]
+// (tokens t, output features f, weights row-major [f][k]).  One kernel
+// template covers them: bf16 MFMA 32x32x16 with fp32 accumulation, output
+// features on the MFMA M side (the weights are the A operand) and tokens on
+// the N side, a 256 x 256 workgroup tile of 8 waves (2 x 4, each 128
+// features x 64 tokens), K steps of 64 whose weight and token slabs are
+// copied HBM -> LDS by global_load_lds_dwordx4 into XOR-swizzled tiles (two
+// stages: the next step's copies fly while the current one is multiplied).
+// The token operand is read either row-major [t][k] or head-major
+// [k / dh][t][dh] (the attention output, whose heads are the O projection's
+// K dimension), so no transpose is ever materialised.  Epilogues:
+//  * row-major bf16 store, plus a residual in fp32 before the rounding;
+//  * head-major Q/K/V store of the QKV projection (feature f is dim f % dh
+//    of head f / dh: Q heads, then K heads, then V heads);
+//  * SwiGLU: each wave's 128 weight rows are 64 gate rows and the 64 up
+//    rows of the same features, so gate and up of one feature sit in the
+//    same lane and register slot and SiLU(gate) * up is formed in registers.
+#include <math.h>
+
+#include "apb_internal.h"
+
+namespace apb {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+
+constexpr int kBF = 256;        // weight rows (output features) per workgroup
+constexpr int kBT = 256;        // tokens per workgroup
+constexpr int kBK = 64;         // K per step
+constexpr int kGemmThreads = 512;
+constexpr int kTileElems = kBF * kBK;  // = kBT * kBK
+
+enum XMode { kXRowMajor = 0, kXHeadMajor = 1 };
+enum WMode { kWPlain = 0, kWGateUp = 1 };
+enum Epi { kEpiRowMajor = 0, kEpiQkv = 1, kEpiSwiglu = 2 };
+
+struct GemmParams {
+  const uint16_t* x;      // tokens: [T][K] or [K / dh][T][dh]
+  const uint16_t* w;      // [F][K]; the gate matrix for kWGateUp
+  const uint16_t* w_up;   // [F][K] for kWGateUp
+  const uint16_t* resid;  // [T][F] or null (kEpiRowMajor)
+  uint16_t* out;          // [T][F] (kEpiRowMajor, kEpiSwiglu); Q for kEpiQkv
+  uint16_t* out_k;        // kEpiQkv: K [n_kv][T][dh]
+  uint16_t* out_v;        // kEpiQkv: V [n_kv][T][dh]
+  int T, K, F;            // F: output features (I for kWGateUp)
+  int dh;                 // head dim of a head-major operand or output
+  int n_q, n_kv;          // kEpiQkv
+};
+
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// 16-byte chunk c of tile row r sits at chunk c ^ (r & 7): the 8 rows one
+// ds_read_b128 pass touches hit 8 different chunk slots.
+__device__ __forceinline__ int swz(int r) { return r & 7; }
+
+template <int XM, int WM, int EPI>
+__global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) uint16_t a_lds[2][kTileElems];  // weight slab
+  __shared__ __attribute__((aligned(16))) uint16_t b_lds[2][kTileElems];  // token slab
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;  // feature half, token quarter
+  const int n = lane & 31, h = lane >> 5;
+  const int t0 = blockIdx.x * kBT;
+  const int f0 = blockIdx.y * (WM == kWGateUp ? kBF / 2 : kBF);
+  const int nk = p.K / kBK;
+
+  // ---- copies: piece j (8 rows x 128 bytes) of each slab; wave w copies
+  // pieces 4w .. 4w+3.  Lane l takes row l/8 of the piece and fetches the
+  // chunk that belongs at slot l%8.  Rows past the last feature or token
+  // repeat it (their results are never stored).
+  const int cp_row = lane >> 3, cp_slot = lane & 7;
+  const uint16_t* w_src[4];
+  const uint16_t* x_src[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rho = 8 * (4 * wave + i) + cp_row;  // slab row 0..255
+    const int chunk = 8 * (cp_slot ^ swz(rho));
+    int fr;
+    const uint16_t* wm_base = p.w;
+    if constexpr (WM == kWGateUp) {
+      const int half = rho >> 7, q = rho & 127;
+      fr = f0 + 64 * half + (q & 63);
+      if (q >= 64) wm_base = p.w_up;
+    } else {
+      fr = f0 + rho;
+    }
+    fr = min(fr, p.F - 1);
+    w_src[i] = wm_base + (size_t)fr * p.K + chunk;
+    const int tr = min(t0 + rho, p.T - 1);
+    if constexpr (XM == kXHeadMajor)
+      x_src[i] = p.x + (size_t)tr * p.dh + chunk;
+    else
+      x_src[i] = p.x + (size_t)tr * p.K + chunk;
+  }
+  auto issue = [&](int kk, int st) __attribute__((always_inline)) {
+    const int k0 = kk * kBK;
+    size_t xoff = (size_t)k0;
+    if constexpr (XM == kXHeadMajor) xoff = (size_t)(k0 / p.dh) * p.T * p.dh + (k0 % p.dh);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = 4 * wave + i;
+      const uint32_t wd = __builtin_amdgcn_readfirstlane(lds_offset(&a_lds[st][j * 512]));
+      const uint32_t xd = __builtin_amdgcn_readfirstlane(lds_offset(&b_lds[st][j * 512]));
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(w_src[i] + k0),
+                   "s"(wd)
+                   : "memory", "m0");
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(x_src[i] + xoff),
+                   "s"(xd)
+                   : "memory", "m0");
+    }
+  };
+
+  // ---- operands: lane (n, h) of an MFMA block reads slab row 32*blk + n,
+  // K elements 16*kc + 8*h .. +7, i.e. chunk 2*kc + h of that row
+  auto a_read = [&](int st, int mb, int kc) __attribute__((always_inline)) -> bf16x8 {
+    const int row = 128 * wm + 32 * mb + n;
+    return *(const lds_bf16x8*)(uintptr_t)(lds_offset(a_lds[st]) + row * 128 +
+                                            16 * ((2 * kc + h) ^ swz(row)));
+  };
+  auto b_read = [&](int st, int nb, int kc) __attribute__((always_inline)) -> bf16x8 {
+    const int row = 64 * wn + 32 * nb + n;
+    return *(const lds_bf16x8*)(uintptr_t)(lds_offset(b_lds[st]) + row * 128 +
+                                            16 * ((2 * kc + h) ^ swz(row)));
+  };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
+
+  issue(0, 0);
+  for (int kk = 0; kk < nk; ++kk) {
+    const int st = kk & 1;
+    // this wave's copies of step kk have landed; after the barrier every
+    // wave's have, and every wave is done reading the other stage
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (kk + 1 < nk) issue(kk + 1, st ^ 1);
+    bf16x8 av[2][4], bv[2][2];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) av[0][mb] = a_read(st, mb, 0);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) bv[0][nb] = b_read(st, nb, 0);
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      const int cur = kc & 1;
+      if (kc + 1 < 4) {
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) av[cur ^ 1][mb] = a_read(st, mb, kc + 1);
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) bv[cur ^ 1][nb] = b_read(st, nb, kc + 1);
+      }
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[cur][mb], bv[cur][nb],
+                                                                acc[mb][nb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // ---- epilogue.  Lane (n, h), block (mb, nb), element r holds slab row
+  // 128*wm + 32*mb + 8*(r/4) + 4*h + r%4 of token t0 + 64*wn + 32*nb + n;
+  // each group of four r is four consecutive features (one 8-byte store).
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int t = t0 + 64 * wn + 32 * nb + n;
+    if (t >= p.T) continue;
+    if constexpr (EPI == kEpiSwiglu) {
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int f = f0 + 64 * wm + 32 * mb + 8 * g + 4 * h;
+          if (f >= p.F) continue;
+          bf16x4 o;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float gt = acc[mb][nb][4 * g + i], up = acc[mb + 2][nb][4 * g + i];
+            o[i] = (__bf16)(gt / (1.f + __expf(-gt)) * up);
+          }
+          *reinterpret_cast<bf16x4*>(p.out + (size_t)t * p.F + f) = o;
+        }
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int f = f0 + 128 * wm + 32 * mb + 8 * g + 4 * h;
+          if (f >= p.F) continue;
+          float v[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = acc[mb][nb][4 * g + i];
+          uint16_t* dst;
+          if constexpr (EPI == kEpiQkv) {
+            const int head = f / p.dh, j = f - head * p.dh;
+            if (head < p.n_q)
+              dst = p.out + ((size_t)head * p.T + t) * p.dh + j;
+            else if (head < p.n_q + p.n_kv)
+              dst = p.out_k + ((size_t)(head - p.n_q) * p.T + t) * p.dh + j;
+            else
+              dst = p.out_v + ((size_t)(head - p.n_q - p.n_kv) * p.T + t) * p.dh + j;
+          } else {
+            dst = p.out + (size_t)t * p.F + f;
+            if (p.resid) {
+              const bf16x4 rr = *reinterpret_cast<const bf16x4*>(p.resid + (size_t)t * p.F + f);
+#pragma unroll
+              for (int i = 0; i < 4; ++i) v[i] += (float)rr[i];
+            }
+          }
+          bf16x4 o;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o[i] = (__bf16)v[i];
+          *reinterpret_cast<bf16x4*>(dst) = o;
+        }
+    }
+  }
+}
+
+// RMSNorm of one row per workgroup: out = in / sqrt(mean(in^2) + eps) * gain,
+// fp32 arithmetic, bf16 in and out.  D % 8 == 0.
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const uint16_t* __restrict__ in,
+                                                      const uint16_t* __restrict__ gain,
+                                                      uint16_t* __restrict__ out, int D,
+                                                      float eps) {
+  __shared__ float red[4];
+  const int tid = threadIdx.x;
+  const uint16_t* row = in + (size_t)blockIdx.x * D;
+  float ss = 0.f;
+  for (int c = 8 * tid; c < D; c += 8 * 256) {
+    const bf16x8 x = *reinterpret_cast<const bf16x8*>(row + c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += (float)x[i] * (float)x[i];
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float inv = 1.f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)D + eps);
+  uint16_t* orow = out + (size_t)blockIdx.x * D;
+  for (int c = 8 * tid; c < D; c += 8 * 256) {
+    const bf16x8 x = *reinterpret_cast<const bf16x8*>(row + c);
+    const bf16x8 g = *reinterpret_cast<const bf16x8*>(gain + c);
+    bf16x8 y;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) y[i] = (__bf16)((float)x[i] * inv * (float)g[i]);
+    *reinterpret_cast<bf16x8*>(orow + c) = y;
+  }
+}
+
+// RoPE in place on head-major Q [n_q][T][dh] and K [n_kv][T][dh]: the pair
+// (j, j + dh/2) of every head rotated by pos[t] * theta^(-2j/dh).  The angle
+// and its cosine and sine are computed in fp64 (positions reach 10^5 and
+// beyond, where an fp32 angle would lose its fraction), the rotation in fp32.
+// One thread per (token, j); it walks all heads with one cos/sin pair.
+__global__ void __launch_bounds__(256) rope_kernel(uint16_t* __restrict__ q,
+                                                   uint16_t* __restrict__ k,
+                                                   const int32_t* __restrict__ pos, int T,
+                                                   int n_q, int n_kv, int dh, double log_theta) {
+  const int half = dh / 2;
+  const int rows_per_block = 256 / half;
+  const int t = blockIdx.x * rows_per_block + threadIdx.x / half;
+  const int j = threadIdx.x % half;
+  if (t >= T) return;
+  const double ang = (double)pos[t] * exp(-2.0 * j / dh * log_theta);
+  const float c = (float)cos(ang), s = (float)sin(ang);
+  for (int hd = 0; hd < n_q + n_kv; ++hd) {
+    uint16_t* base = hd < n_q ? q + ((size_t)hd * T + t) * dh : k + ((size_t)(hd - n_q) * T + t) * dh;
+    __bf16* x = reinterpret_cast<__bf16*>(base);
+    const float lo = (float)x[j], hi = (float)x[j + half];
+    x[j] = (__bf16)(lo * c - hi * s);
+    x[j + half] = (__bf16)(hi * c + lo * s);
+  }
+}
+
+template <int XM, int WM, int EPI>
+hipError_t launch_gemm(const GemmParams& p, hipStream_t stream) {
+  const int per_wg = WM == kWGateUp ? kBF / 2 : kBF;
+  const dim3 grid((unsigned)((p.T + kBT - 1) / kBT), (unsigned)((p.F + per_wg - 1) / per_wg));
+  hipLaunchKernelGGL((gemm_kernel<XM, WM, EPI>), grid, dim3(kGemmThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+// Workspace carve-up (256-byte aligned pieces).
+struct LayerPlan {
+  uint64_t x, q, attn, h1, act, scorer, scores, idx, total;
+};
+
+uint64_t align256(uint64_t b) { return (b + 255) & ~uint64_t(255); }
+
+LayerPlan plan_layer(const LayerArgs& a) {
+  LayerPlan pl;
+  const uint64_t T = (uint64_t)a.La + a.Lb;
+  uint64_t off = 0;
+  auto take = [&](uint64_t bytes) {
+    const uint64_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  pl.x = take(T * a.D * 2);
+  pl.q = take((uint64_t)a.n_q * T * a.head_dim * 2);
+  pl.attn = take((uint64_t)a.n_q * T * a.head_dim * 2);
+  pl.h1 = take(T * a.D * 2);
+  pl.act = take(T * a.I * 2);
+  ScorerArgs sa{};
+  sa.La = a.La; sa.Lb = a.Lb; sa.n_q = a.n_q; sa.n_kv = a.n_kv; sa.head_dim = a.head_dim;
+  sa.hidden = a.scorer_hidden;
+  pl.scorer = take(scorer_workspace_bytes(sa));
+  pl.scores = take((uint64_t)a.n_kv * a.Lb * 4);
+  pl.idx = take((uint64_t)a.n_kv * (a.lp > 0 ? a.lp : 1) * 4);
+  pl.total = off;
+  return pl;
+}
+
+}  // namespace
+
+uint64_t layer_workspace_bytes(const LayerArgs& a) { return plan_layer(a).total; }
+
+hipError_t launch_layer(const LayerArgs& a, hipStream_t stream) {
+  const LayerPlan pl = plan_layer(a);
+  uint8_t* ws = static_cast<uint8_t*>(a.workspace);
+  uint16_t* x = reinterpret_cast<uint16_t*>(ws + pl.x);
+  uint16_t* q = reinterpret_cast<uint16_t*>(ws + pl.q);
+  uint16_t* attn = reinterpret_cast<uint16_t*>(ws + pl.attn);
+  uint16_t* h1 = reinterpret_cast<uint16_t*>(ws + pl.h1);
+  uint16_t* act = reinterpret_cast<uint16_t*>(ws + pl.act);
+  float* scores = reinterpret_cast<float*>(ws + pl.scores);
+  int32_t* idx = reinterpret_cast<int32_t*>(ws + pl.idx);
+  const int T = a.La + a.Lb, d = a.head_dim;
+  hipError_t e;
+
+  // 1. x = RMSNorm(H; g1)
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(256), 0, stream, a.hidden, a.ln1, x,
+                     a.D, a.eps);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // 2. Q, K, V = x W_qkv^T (head-major), then RoPE on Q and K
+  GemmParams g{};
+  g.x = x; g.w = a.w_qkv; g.out = q; g.out_k = a.k_cache; g.out_v = a.v_cache;
+  g.T = T; g.K = a.D; g.F = (a.n_q + 2 * a.n_kv) * d; g.dh = d; g.n_q = a.n_q; g.n_kv = a.n_kv;
+  if ((e = launch_gemm<kXRowMajor, kWPlain, kEpiQkv>(g, stream)) != hipSuccess) return e;
+  {
+    const int rpb = 256 / (d / 2);
+    hipLaunchKernelGGL(rope_kernel, dim3((unsigned)((T + rpb - 1) / rpb)), dim3(256), 0, stream, q,
+                       a.k_cache, a.pos, T, a.n_q, a.n_kv, d, log((double)a.theta));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  // 3. retaining-head scores of the local block, ArgTop-l_p and gather into
+  //    this host's slot of the passing buffer
+  {
+    ScorerArgs sa{};
+    sa.q = q; sa.k = a.k_cache; sa.v = a.v_cache; sa.w1 = a.r_w1; sa.b1 = a.r_b1; sa.w2 = a.r_w2;
+    sa.b2 = a.r_b2; sa.scores = scores; sa.workspace = reinterpret_cast<float*>(ws + pl.scorer);
+    sa.La = a.La; sa.Lb = a.Lb; sa.n_q = a.n_q; sa.n_kv = a.n_kv; sa.head_dim = d;
+    sa.hidden = a.scorer_hidden;
+    if ((e = launch_scorer(sa, stream)) != hipSuccess) return e;
+  }
+  if (a.lp > 0) {
+    const size_t slot = (size_t)a.host_idx * a.n_kv * a.lp * d;
+    CompressArgs ca;
+    ca.scores = scores; ca.k = a.k_cache; ca.v = a.v_cache; ca.idx = idx;
+    ca.out_k = a.pass_k + slot; ca.out_v = a.pass_v + slot;
+    ca.La = a.La; ca.Lb = a.Lb; ca.lp = a.lp; ca.n_kv = a.n_kv; ca.head_dim = d;
+    if ((e = launch_compress(ca, stream)) != hipSuccess) return e;
+  }
+  // 4. attention over [A; P; B] reading the earlier hosts' slots in place
+  {
+    AttnArgs aa;
+    const int Lp = a.host_idx * a.lp;
+    aa.q = q; aa.k = a.k_cache; aa.v = a.v_cache;
+    aa.kp = Lp > 0 ? a.pass_k : nullptr;
+    aa.vp = Lp > 0 ? a.pass_v : nullptr;
+    aa.o = attn; aa.lse = nullptr;
+    aa.La = a.La; aa.Lb = a.Lb; aa.lp = a.lp; aa.Lp = Lp;
+    aa.n_q = a.n_q; aa.n_kv = a.n_kv; aa.head_dim = d;
+    aa.scale_log2 = 1.4426950408889634f / sqrtf((float)d);
+    if ((e = launch_attention(aa, stream)) != hipSuccess) return e;
+  }
+  // 5. H1 = H + concat_heads(A) W_o^T
+  g = GemmParams{};
+  g.x = attn; g.w = a.w_o; g.resid = a.hidden; g.out = h1;
+  g.T = T; g.K = a.n_q * d; g.F = a.D; g.dh = d;
+  if ((e = launch_gemm<kXHeadMajor, kWPlain, kEpiRowMajor>(g, stream)) != hipSuccess) return e;
+  // 6. y = RMSNorm(H1; g2) (into the x buffer)
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(256), 0, stream, h1, a.ln2, x, a.D,
+                     a.eps);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // 7. act = SiLU(y W_gate^T) * (y W_up^T)
+  g = GemmParams{};
+  g.x = x; g.w = a.w_gate; g.w_up = a.w_up; g.out = act; g.T = T; g.K = a.D; g.F = a.I;
+  if ((e = launch_gemm<kXRowMajor, kWGateUp, kEpiSwiglu>(g, stream)) != hipSuccess) return e;
+  // 8. out = H1 + act W_down^T
+  g = GemmParams{};
+  g.x = act; g.w = a.w_down; g.resid = h1; g.out = a.hidden_out; g.T = T; g.K = a.I; g.F = a.D;
+  return launch_gemm<kXRowMajor, kWPlain, kEpiRowMajor>(g, stream);
+}
+
+}  // namespace apb

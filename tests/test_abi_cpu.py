@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(apb.EXPORTED)
     for name in declared:
         assert hasattr(L, name), name
-    assert apb.abi_version() == 3
+    assert apb.abi_version() == 4
 
 
 def _prob(**kw):
@@ -277,3 +277,86 @@ def test_probe_library_exports_and_validates():
     for args in [(None, fake, 1, 8), (fake, None, 1, 8), (fake, fake, 0, 8), (fake, fake, 1, 0),
                  (fake, fake, 1, 12), (fake + 8, fake, 1, 8), (fake, fake, 1, (1 << 20) + 8)]:
         assert L.apb_probe_mfma_bf16(*args, None) == 1, args
+
+
+# ------------------------------------------------------------ whole layer
+def _lprob(**kw):
+    lw = inputs.LAYER_WORKLOADS["tiny_layer"]
+    base = dict(hidden=lw.hidden, intermediate=lw.intermediate, scorer_hidden=lw.scorer_hidden,
+                rms_eps=lw.eps, rope_theta=lw.theta)
+    attn = {k: kw.pop(k) for k in list(kw) if k in dict(apb.Problem._fields_)}
+    base.update(kw)
+    return apb.LayerProblem(_prob(**attn), **base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), 0),
+    (dict(hidden=96), 2),
+    (dict(hidden=0), 2),
+    (dict(intermediate=100), 2),
+    (dict(rms_eps=0.0), 2),
+    (dict(rms_eps=float("nan")), 2),
+    (dict(rope_theta=1.0), 2),
+    (dict(rope_theta=float("inf")), 2),
+    (dict(scorer_hidden=100), 3),          # the retaining head's hidden block
+    (dict(head_dim=96), 3),
+    (dict(pass_len=600), 2),
+    (dict(n_q_heads=18, n_kv_heads=9), 3),  # more KV heads than the fused scorer takes
+])
+def test_validate_layer(kw, code):
+    assert apb.validate_layer(_lprob(**kw)) == code
+
+
+def test_layer_flops_and_workspace():
+    for lw in inputs.LAYER_WORKLOADS.values():
+        p = lw.problem
+        attn = oracle.attention_flops(p.n_q_heads, p.head_dim, p.anchor_len, p.local_len,
+                                      p.passing_rows)
+        sc = oracle.scorer_flops(p.n_q_heads, p.n_kv_heads, p.head_dim, p.local_len,
+                                 lw.scorer_hidden)
+        ref = oracle.layer_flops(p.rows, lw.hidden, lw.intermediate, p.n_q_heads, p.n_kv_heads,
+                                 p.head_dim, attn, sc)
+        assert apb.layer_flops(lw) == pytest.approx(ref, rel=1e-12)
+        ws = apb.layer_workspace_size(lw)
+        # at least x, Q, A, H1 (bf16) and the SwiGLU product
+        T, D = p.rows, lw.hidden
+        assert ws >= 2 * (2 * T * D + 2 * p.n_q_heads * T * p.head_dim + T * lw.intermediate)
+    assert apb.lib().apb_layer_flops(ctypes.byref(_lprob(hidden=96))) == -1.0
+
+
+LW = {n: A + (11 + i) * (1 << 36) for i, n in enumerate(
+    ("ln1", "w_qkv", "w_o", "ln2", "w_gate", "w_up", "w_down", "r_w1", "r_b1", "r_w2", "r_b2"))}
+HIN, POS, KC, VC, PK, PV, HOUT, WS = (A + (22 + i) * (1 << 36) for i in range(8))
+
+
+def _layer(p, ws_bytes=1 << 40, w=None, **kw):
+    args = dict(hin=HIN, pos=POS, kc=KC, vc=VC, pk=PK, pv=PV, hout=HOUT, ws=WS)
+    args.update(kw)
+    ww = apb.LayerWeights(**(w or LW))
+    return apb.lib().apb_layer_fwd(ctypes.byref(p), ctypes.byref(ww), args["hin"], args["pos"],
+                                   args["kc"], args["vc"], args["pk"], args["pv"], args["hout"],
+                                   args["ws"], ws_bytes, None)
+
+
+def test_layer_error_paths():
+    p = _lprob()
+    ww = apb.LayerWeights(**LW)
+    assert apb.lib().apb_layer_fwd(None, ctypes.byref(ww), HIN, POS, KC, VC, PK, PV, HOUT, WS,
+                                   1 << 40, None) == 1
+    assert _layer(p, hin=None) == 1
+    assert _layer(p, pk=None) == 1                    # l_p > 0 needs the passing buffers
+    assert _layer(p, w=dict(LW, w_up=None)) == 1
+    assert _layer(p, w=dict(LW, r_b2=None)) == 1
+    assert _layer(p, hout=HOUT + 8) == 4
+    assert _layer(p, w=dict(LW, w_down=LW["w_down"] + 2)) == 4
+    assert _layer(p, pos=POS + 2) == 4
+    assert _layer(p, ws_bytes=16) == 2                # workspace too small
+    assert _layer(p, hout=HIN) == 6                   # output over an input
+    assert _layer(p, kc=LW["w_qkv"] + 256) == 6
+    assert _layer(p, vc=KC + 64) == 6                 # outputs over each other
+    assert _layer(p, ws=HOUT + 16) == 6
+    # this host's slot (host_idx = 2) is written; the earlier slots are read
+    slot = 1 * 32 * 64 * 2
+    assert _layer(p, kc=PK + slot) == 6               # the KV cache over a read slot
+    assert _layer(p, hout=PK + 2 * slot) == 6         # an output over the written slot
+    assert _layer(_lprob(head_dim=96)) == 3
