@@ -20,7 +20,9 @@
 //    ds_read_b128 as the A operand of S^T; V is read back transposed with
 //    ds_read_b64_tr_b16 as the A operand of O^T = V^T P^T, and P comes
 //    straight from the S^T accumulator layout.
-//  * Online softmax in base 2 in fp32, P rounded to bf16 for the PV MFMA.
+//  * Online softmax in base 2 in fp32 with a lazily moved running max (the
+//    max pass and the O rescale only when a block sum passes 2^13), P
+//    rounded to bf16 for the PV MFMA.
 //
 // MergeScore.  lse = m + ln sum_p exp(lse_p - m), A = sum_p exp(lse_p - lse)
 // A_p with m the largest lse_p; parts with lse = -inf add nothing; a row
@@ -44,6 +46,7 @@ constexpr int kRows = 32;   // rows per workgroup (the MFMA N side)
 constexpr int kKeys = 32;   // keys per block (the MFMA M side)
 constexpr int kRing = 3;    // LDS stages of K and V blocks per workgroup
 constexpr int kWgPerCu = 3; // workgroups per CU (LDS: 3 x 48 KiB at d = 128)
+constexpr float kSumLimit = 8192.f;  // lazy rescale: largest block row-half sum against a stale max
 
 struct DecParams {
   const uint16_t* q;
@@ -83,8 +86,12 @@ __device__ __forceinline__ const uint16_t* kv_row(const DecParams& p, const uint
                   : fresh + ((size_t)kvh * p.n_new + (c - p.Lc)) * D;
 }
 
-template <int D>
-__global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
+// W waves per workgroup share one K/V ring: wave w owns 32-row block
+// W * blockIdx.z + w.  W = 1 for few rows (one generated token); W = 8 when a
+// GQA group has many rows (the question tokens), so that each K/V block is
+// copied once for 256 rows instead of once per 32.
+template <int D, int W>
+__global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
   constexpr int NKC = D / 16;                // MFMA k-steps over head_dim
   constexpr int NDB = D / 32;                // 32-dim blocks of O^T
   constexpr int KCH = D / 8;                 // 16-byte chunks per row
@@ -94,8 +101,13 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kRing][kKeys * D];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[kRing][kKeys * D];
 
-  const int lane = threadIdx.x, n = lane & 31, h = lane >> 5;
-  const int split = blockIdx.x, kvh = blockIdx.y, rb = blockIdx.z;
+  const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
+  const int wave = W == 1 ? 0 : __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int split = blockIdx.x, kvh = blockIdx.y, rb = blockIdx.z * W + wave;
+  // copies per wave per block: all 2 * PIECES for one wave, else this
+  // wave's share (pieces w, w + W, ... of the K tile, then of the V tile)
+  constexpr int CPW = 2 * PIECES / W;
+  static_assert(CPW * W == 2 * PIECES && CPW >= 1, "pieces split evenly over the waves");
   const int Ltot = p.Lc + (p.append ? p.n_new : 0);
   const int nblk = (Ltot + kKeys - 1) / kKeys;
   const int b0 = split * p.blocks_per_split;
@@ -149,7 +161,42 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
     k_off[j] = 2u * (uint32_t)(row * D + 8 * (cp_slot ^ k_swz<D>(row))) - 1024u * (j & 3);
     v_off[j] = 2u * (uint32_t)(row * D + 8 * (cp_slot ^ v_swz<D>(row))) - 1024u * (j & 3);
   }
+  // W > 1: this wave's copies, piece q = wave + W*i of the 2*PIECES pieces
+  // (K pieces first, then V): one scalar base and one M0 per piece
+  auto load_share = [&](int b, int buf) __attribute__((always_inline)) {
+    const int c0 = b * kKeys;
+    const bool in_cache = c0 + kKeys <= p.Lc;
+    const bool in_new = c0 >= p.Lc && c0 + kKeys <= Ltot;
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int q = wave + W * i;
+      const bool is_v = q >= PIECES;
+      const int j = is_v ? q - PIECES : q;
+      const int row = j * ROWS_PER_PIECE + cp_row0;
+      const int swz = is_v ? v_swz<D>(row) : k_swz<D>(row);
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(
+          lds_offset(is_v ? &v_lds[buf][j * 512] : &k_lds[buf][j * 512]));
+      if (in_cache || in_new) {
+        const size_t r0 = in_cache ? (size_t)kvh * p.Lc + c0 : (size_t)kvh * p.n_new + (c0 - p.Lc);
+        const uint16_t* base = (is_v ? (in_cache ? p.vc : p.vn) : (in_cache ? p.kc : p.kn)) + r0 * D;
+        const uint32_t off = 2u * (uint32_t)(row * D + 8 * (cp_slot ^ swz));
+        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
+                     "s"(dst)
+                     : "memory");
+      } else {
+        const int c = min(c0 + row, Ltot - 1);
+        const uint16_t* src = kv_row<D>(p, is_v ? p.vc : p.kc, is_v ? p.vn : p.kn, kvh, c) +
+                              8 * (cp_slot ^ swz);
+        asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst)
+                     : "memory");
+      }
+    }
+  };
   auto load_block = [&](int b, int buf) __attribute__((always_inline)) {
+    if constexpr (W > 1) {
+      load_share(b, buf);
+      return;
+    }
     const int c0 = b * kKeys;
     const uint32_t kd = __builtin_amdgcn_readfirstlane(lds_offset(k_lds[buf]));
     const uint32_t vd = __builtin_amdgcn_readfirstlane(lds_offset(v_lds[buf]));
@@ -207,15 +254,20 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
   for (int b = b0; b < b1; ++b) {
     const int buf = (b - b0) % kRing;
     // block b has landed once at most block b+1's copies are outstanding
-    // (this wave is the workgroup: its own wait suffices); then block b+2
+    // (with one wave its own wait suffices, with W the barrier below); then block b+2
     // goes into the stage block b-1 used, whose reads ended with the
     // previous iteration
     if (b + 1 < b1) {
-      if constexpr (PIECES == 8) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      if constexpr (CPW == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      else if constexpr (CPW == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      else if constexpr (CPW == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(1)" ::: "memory");
     } else {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     }
+    // every wave's copies of block b have landed, and every wave is done
+    // with block b-1, whose stage block b+2 reuses
+    if constexpr (W > 1) asm volatile("s_barrier" ::: "memory");
     if (b + 2 < b1) load_block(b + 2, (b - b0 + 2) % kRing);
     const uint32_t kl = lds_offset(k_lds[buf]);
     bf16x8 kop[NKC];
@@ -226,38 +278,58 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc)
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qreg[kc], s, 0, 0, 0);
-    // mask: element r of this lane is key b*32 + 8*(r/4) + 4*h + r%4 of row rho
+    // mask: element r of this lane is key b*32 + 8*(r/4) + 4*h + r%4 of row
+    // rho; only blocks that reach past the cache can hide keys
     const int c0 = b * kKeys;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
-      if (c >= vis) s[r] = -INFINITY;
-    }
-    float mx = s[0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
-    mx = fmaxf(mx, half_swap(mx));
-    const float m_new = fmaxf(m_run, mx * p.scale_log2);
-    bf16x8 pb[2];
-    if (m_new == -INFINITY) {  // nothing visible yet in this row
-#pragma unroll
-      for (int r = 0; r < 16; ++r) pb[r >> 3][r & 7] = (__bf16)0.f;
-    } else {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // m_run = -inf gives 0
-      m_run = m_new;
-      float rs = 0.f;
+    if (c0 + kKeys > p.Lc) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -m_new));
-        rs += e;
-        pb[r >> 3][r & 7] = (__bf16)e;
+        const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (c >= vis) s[r] = -INFINITY;
       }
-      l_run = l_run * alpha + rs;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
     }
+    // Lazy running max (as in the prefill kernel): the probabilities are
+    // formed against the current m_run, and only when some row-half's block
+    // sum exceeds kSumLimit (a logit far above m_run, or a row's first
+    // visible block, where m_run = -inf and the sum is not finite) does the
+    // wave take the block max, raise m_run, rescale O and l and redo the
+    // block.  A row that sees no key yet keeps m_run = -inf and P = 0.
+    bf16x8 pb[2];
+    float rs;
+    auto exp_block = [&]() __attribute__((always_inline)) {
+      float e[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -m_run));
+      float r4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r4[j] = (e[j] + e[4 + j]) + (e[8 + j] + e[12 + j]);
+      rs = (r4[0] + r4[1]) + (r4[2] + r4[3]);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pb[r >> 3][r & 7] = (__bf16)e[r];
+    };
+    exp_block();
+    if (__any(!(rs <= kSumLimit))) {
+      float mx = s[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+      mx = fmaxf(mx, half_swap(mx));
+      const float m_new = fmaxf(m_run, mx * p.scale_log2);
+      if (m_new == -INFINITY) {  // nothing visible yet in this row
+        rs = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pb[r >> 3][r & 7] = (__bf16)0.f;
+      } else {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // m_run = -inf gives 0
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+        exp_block();
+      }
+    }
+    l_run += rs;
     // O^T += V^T P^T: the V tile of block b is in LDS (waited for above)
     const uint32_t vb = lds_offset(v_lds[buf]);
 #pragma unroll
@@ -388,9 +460,13 @@ DecodePlan plan_decode(const DecodeArgs& a) {
   const int64_t keys = (int64_t)a.Lc + (a.append ? a.n_new : 0);
   const int64_t nblk = (keys + kKeys - 1) / kKeys;
   const int64_t R = (int64_t)(a.n_q / a.n_kv) * a.n_new;
-  const int64_t n_rb = (R + kRows - 1) / kRows;
-  // one round of workgroups at kWgPerCu per CU, at least two key blocks each
-  const int64_t target = 256 * kWgPerCu;
+  // a GQA group of at least four 32-row blocks shares each K/V block among
+  // the 8 waves of a workgroup (one workgroup per CU: its registers), else
+  // one wave per workgroup (kWgPerCu per CU: their LDS)
+  pl.waves = R >= 4 * kRows ? 8 : 1;
+  const int64_t n_rb = (R + kRows * pl.waves - 1) / (kRows * pl.waves);
+  // one round of workgroups, at least two key blocks each
+  const int64_t target = pl.waves == 1 ? 256 * kWgPerCu : 256;
   int64_t n_split = target / (a.n_kv * n_rb);
   if (n_split > nblk / 2) n_split = nblk / 2;
   if (n_split < 1) n_split = 1;
@@ -417,10 +493,14 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
   p.blocks_per_split = pl.blocks_per_split;
   p.scale_log2 = a.scale_log2;
   const dim3 grid((unsigned)pl.n_split, (unsigned)a.n_kv, (unsigned)pl.row_blocks);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(decode_partial_kernel<128>, grid, dim3(64), 0, stream, p);
-  else
-    hipLaunchKernelGGL(decode_partial_kernel<64>, grid, dim3(64), 0, stream, p);
+  const dim3 block((unsigned)(64 * pl.waves));
+  if (a.head_dim == 128) {
+    if (pl.waves == 8) hipLaunchKernelGGL((decode_partial_kernel<128, 8>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((decode_partial_kernel<128, 1>), grid, block, 0, stream, p);
+  } else {
+    if (pl.waves == 8) hipLaunchKernelGGL((decode_partial_kernel<64, 8>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((decode_partial_kernel<64, 1>), grid, block, 0, stream, p);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_merge_t<float>(pl.n_split, (int)rows_total, a.head_dim, p.part_o, p.part_lse,

@@ -56,7 +56,8 @@ struct DecodeArgs {
 struct DecodePlan {
   int n_split;
   int blocks_per_split;
-  int row_blocks;
+  int row_blocks;      // workgroups along the rows (each waves * 32 rows)
+  int waves;           // waves per workgroup sharing one K/V ring (1 or 8)
   uint64_t workspace_bytes;
 };
 

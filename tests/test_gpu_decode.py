@@ -4,7 +4,8 @@ fp64 oracle: one host's partial attention (fp32 output, LSE) and MergeScore.
 Bar: the attention bar (output max-abs 2e-2, mean-abs 2e-3; LSE max-abs
 1e-3).  Cases span several 32-key blocks and splits with ragged tails, both
 head sizes, an empty cache, more rows than one 32-row block, every host of a
-simulated decoding step, and the full-size 128K Llama-8B-shaped step (every
+simulated decoding step, GQA groups of 128 rows and more (where eight waves
+share each K/V block), and the full-size 128K Llama-8B-shaped steps (every
 row: a decoding step has only n_q * n_new rows).
 """
 import numpy as np
@@ -45,6 +46,12 @@ def _run_decode(q, kc, vc, kn, vn, n_q, n_kv, d, scale=0.0):
     (12, 2, 128, 777, 17, 1),     # 102 rows per KV head: four 32-row blocks
     (7, 7, 64, 3000, 40, 0),      # no GQA, 40 rows
     (56, 8, 128, 4100, 2, 1),     # Yi-shaped group of 7
+    # >= 128 rows per KV head: 8 waves share each K/V block
+    (8, 2, 64, 1000, 40, 1),      # 160 rows: one partly filled 256-row group, d = 64
+    (16, 2, 128, 2000, 40, 1),    # 320 rows: two row groups, the second ragged
+    (4, 4, 128, 513, 130, 1),     # no GQA, 130 causal new tokens over a ragged cache
+    (8, 2, 128, 0, 64, 1),        # empty cache, 256 rows of new tokens alone
+    (56, 8, 128, 100, 20, 0),     # few keys (four blocks), 140 rows, no append
 ])
 def test_decode_matches_oracle(shape):
     n_q, n_kv, d, lc, n_new, app = shape
