@@ -3,9 +3,11 @@
 
 One step = the whole host-share hot path on one batch of synthetic input:
 ``apb_compress_select`` (top-l_p of the local block's scores + gather into
-slot host_idx of the rank-major passing buffer) followed by
-``apb_attention_fwd`` (modified-mask attention reading the earlier hosts'
-slots in place).  Inputs are resident in HBM before timing starts.
+slot host_idx of the rank-major passing buffer) and ``apb_attention_fwd``
+(modified-mask attention reading the earlier hosts' slots in place).  The
+compressor's output is not read by the same host's attention, so the two run
+concurrently on two streams (``--serial``: back to back on one).  Inputs are
+resident in HBM before timing starts.
 
 Prints ONE JSON line.  ``value`` is unmasked attention TFLOP/s over the
 whole step; ``roofline`` reports the attention kernel alone (HIP events on
@@ -345,6 +347,8 @@ def main():
                     help="skip the decoding-stage (Alg. 3) measurement")
     ap.add_argument("--no-scorer", action="store_true",
                     help="skip the retaining-head scorer measurement")
+    ap.add_argument("--serial", action="store_true",
+                    help="run the compressor and the attention back to back on one stream")
     ap.add_argument("--no-layer", action="store_true",
                     help="skip the whole-layer (Alg. 2) measurement")
     ap.add_argument("--no-ceiling", action="store_true",
@@ -401,18 +405,31 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    # This host's compressor writes slot host_idx, which its own attention
+    # does not read (it reads slots < host_idx): the two kernels run
+    # concurrently, the compressor on a second stream (default priority);
+    # --serial runs them back to back on one stream.
+    side = torch.cuda.Stream()
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(5))
+          for _ in range(args.steps)]
 
     def step(events=None):
+        start = events[0] if events else torch.cuda.Event()
+        start.record(stream)
+        cs = stream if args.serial else side
+        if not args.serial:
+            cs.wait_event(start)
         if events:
-            events[0].record(stream)
-        apb.compress_select(p, scores, k, v, idx, kbuf[p.host_idx], vbuf[p.host_idx], stream)
+            events[1].record(cs)
+        apb.compress_select(p, scores, k, v, idx, kbuf[p.host_idx], vbuf[p.host_idx], cs)
         if events:
-            events[1].record(stream)
+            events[2].record(cs)
+            events[3].record(stream)
         apb.attention_fwd(p, q, k, v, kbuf, vbuf, o, lse, 0.0, stream)
         if events:
-            events[2].record(stream)
+            events[4].record(stream)
+        if not args.serial:
+            stream.wait_stream(side)
 
     for _ in range(args.warmup):
         step()
@@ -437,8 +454,8 @@ def main():
     del flush
     cold_us = 1e3 * sorted(a.elapsed_time(b) for a, b in cold)[len(cold) // 2]
 
-    comp_ms = [a.elapsed_time(b) for a, b, _ in ev]
-    attn_ms = [b.elapsed_time(c) for _, b, c in ev]
+    comp_ms = [e[1].elapsed_time(e[2]) for e in ev]
+    attn_ms = [e[3].elapsed_time(e[4]) for e in ev]
     ms_step = wall * 1e3 / args.steps
     flops = apb.attention_flops(p)
     attn_avg = sum(attn_ms) / len(attn_ms)
@@ -469,6 +486,8 @@ def main():
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "tokens_per_s": round(p.rows / (ms_step * 1e-3), 1),
         "attention_ms": round(attn_avg, 4),
+        "step_schedule": ("compressor then attention, one stream" if args.serial else
+                          "compressor on a second stream, concurrent with the attention"),
         "compress_us": round(1e3 * sum(comp_ms) / len(comp_ms), 2),
         "compress_gbs": round(comp_bytes / (sum(comp_ms) / len(comp_ms) * 1e-3) / 1e9, 1),
         "compress_cold_us": round(cold_us, 2),
