@@ -5,8 +5,8 @@ One step = the whole host-share hot path on one batch of synthetic input:
 ``apb_compress_select`` (top-l_p of the local block's scores + gather into
 slot host_idx of the rank-major passing buffer) and ``apb_attention_fwd``
 (modified-mask attention reading the earlier hosts' slots in place).  The
-compressor's output is not read by the same host's attention, so the two run
-concurrently on two streams (``--serial``: back to back on one).  Inputs are
+compressor's output is not read by the same host's attention; they run back
+to back on one stream (``--overlap``: concurrently on two).  Inputs are
 resident in HBM before timing starts.
 
 Prints ONE JSON line.  ``value`` is unmasked attention TFLOP/s over the
@@ -347,8 +347,8 @@ def main():
                     help="skip the decoding-stage (Alg. 3) measurement")
     ap.add_argument("--no-scorer", action="store_true",
                     help="skip the retaining-head scorer measurement")
-    ap.add_argument("--serial", action="store_true",
-                    help="run the compressor and the attention back to back on one stream")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run the compressor on a second stream, concurrent with the attention")
     ap.add_argument("--no-layer", action="store_true",
                     help="skip the whole-layer (Alg. 2) measurement")
     ap.add_argument("--no-ceiling", action="store_true",
@@ -406,9 +406,9 @@ def main():
 
     stream = torch.cuda.current_stream()
     # This host's compressor writes slot host_idx, which its own attention
-    # does not read (it reads slots < host_idx): the two kernels run
-    # concurrently, the compressor on a second stream (default priority);
-    # --serial runs them back to back on one stream.
+    # does not read (it reads slots < host_idx): --overlap runs the
+    # compressor on a second stream (default priority) concurrently with the
+    # attention; by default they run back to back on one stream.
     side = torch.cuda.Stream()
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(5))
           for _ in range(args.steps)]
@@ -416,8 +416,8 @@ def main():
     def step(events=None):
         start = events[0] if events else torch.cuda.Event()
         start.record(stream)
-        cs = stream if args.serial else side
-        if not args.serial:
+        cs = side if args.overlap else stream
+        if args.overlap:
             cs.wait_event(start)
         if events:
             events[1].record(cs)
@@ -428,7 +428,7 @@ def main():
         apb.attention_fwd(p, q, k, v, kbuf, vbuf, o, lse, 0.0, stream)
         if events:
             events[4].record(stream)
-        if not args.serial:
+        if args.overlap:
             stream.wait_stream(side)
 
     for _ in range(args.warmup):
@@ -486,8 +486,8 @@ def main():
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "tokens_per_s": round(p.rows / (ms_step * 1e-3), 1),
         "attention_ms": round(attn_avg, 4),
-        "step_schedule": ("compressor then attention, one stream" if args.serial else
-                          "compressor on a second stream, concurrent with the attention"),
+        "step_schedule": ("compressor on a second stream, concurrent with the attention"
+                          if args.overlap else "compressor then attention, one stream"),
         "compress_us": round(1e3 * sum(comp_ms) / len(comp_ms), 2),
         "compress_gbs": round(comp_bytes / (sum(comp_ms) / len(comp_ms) * 1e-3) / 1e9, 1),
         "compress_cold_us": round(cold_us, 2),

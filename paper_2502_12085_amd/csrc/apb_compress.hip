@@ -168,10 +168,183 @@ topk_gather_kernel(const float* __restrict__ scores, const uint16_t* __restrict_
   }
 }
 
+// ---------------------------------------------------------------------------
+// Register-resident variant for Lb <= 1024 * KPT (KPT <= 32 keeps the keys in
+// registers without spills; longer local blocks use the kernel above).
+// 1024 threads; thread t
+// holds the keys of local indices KPT*t .. KPT*t + KPT-1 in registers, loaded
+// once with 16-byte vector loads.  The radix select counts into one 256-bin
+// histogram per wave (LDS atomics collide only within a wave) and sums the
+// sixteen of them; the selected counts before each thread's range come from a
+// block scan.  Workgroup c of a head then gathers the selected rows whose
+// output positions fall in its share [c*lp/S, (c+1)*lp/S).  Same threshold,
+// same tie rule, same output as the kernel above.
+constexpr int kRegThreads = 1024;
+constexpr int kRegWaves = kRegThreads / 64;
+
+template <int KPT>
+__global__ void __launch_bounds__(kRegThreads)
+topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restrict__ k,
+                       const uint16_t* __restrict__ v, int32_t* __restrict__ out_idx,
+                       uint16_t* __restrict__ out_k, uint16_t* __restrict__ out_v, int La,
+                       int Lb, int lp, int head_dim, int share) {
+  __shared__ uint32_t hist[kRegWaves][256];
+  __shared__ uint32_t wsum_gt[kRegWaves], wsum_eq[kRegWaves];
+  __shared__ uint32_t sel_digit, sel_above;
+  __shared__ int32_t list_src[1024];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int head = blockIdx.y;
+  const float* s = scores + (size_t)head * Lb;
+  const int i0 = KPT * tid;
+
+  // ---- keys in registers; indices past Lb are marked invalid
+  uint32_t key[KPT];
+  if (i0 + KPT <= Lb && ((uintptr_t)s & 15u) == 0) {
+#pragma unroll
+    for (int j = 0; j < KPT; j += 4) {
+      const float4 f = *reinterpret_cast<const float4*>(s + i0 + j);
+      key[j] = score_key(f.x); key[j + 1] = score_key(f.y);
+      key[j + 2] = score_key(f.z); key[j + 3] = score_key(f.w);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) key[j] = i0 + j < Lb ? score_key(s[i0 + j]) : 0u;
+  }
+  const int n_valid = max(0, min(KPT, Lb - i0));
+
+  // every share slot is filled below (exactly lp distinct positions are
+  // selected); -1 marks a slot as empty for the gather regardless
+  list_src[tid] = -1;
+
+  // ---- 1. radix select: key T of the lp-th largest score and `need`
+  uint32_t prefix = 0u, prefix_mask = 0u, remaining = (uint32_t)lp;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int b = lane; b < 256; b += 64) hist[wave][b] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < KPT; ++j)
+      if (j < n_valid && (key[j] & prefix_mask) == prefix)
+        atomicAdd(&hist[wave][(key[j] >> shift) & 255u], 1u);
+    __syncthreads();
+    if (tid < 64) {
+      // lane L owns bins 4L..4L+3 (summed over the waves' histograms)
+      uint32_t c[4], own = 0u;
+      for (int j = 0; j < 4; ++j) {
+        uint32_t t = 0u;
+        for (int w = 0; w < kRegWaves; ++w) t += hist[w][4 * lane + j];
+        c[j] = t;
+        own += t;
+      }
+      uint32_t incl = own;  // inclusive suffix sum over lanes >= lane
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = __shfl_down(incl, off);
+        if (lane + off < 64) incl += o;
+      }
+      const uint32_t above_lane = incl - own;
+      if (above_lane < remaining && remaining <= incl) {
+        uint32_t above = above_lane;
+        for (int j = 3; j >= 0; --j) {
+          if (remaining <= above + c[j]) {
+            sel_digit = (uint32_t)(4 * lane + j);
+            sel_above = above;
+            break;
+          }
+          above += c[j];
+        }
+      }
+    }
+    __syncthreads();
+    prefix |= sel_digit << shift;
+    prefix_mask |= 255u << shift;
+    remaining -= sel_above;
+    __syncthreads();
+  }
+  const uint32_t T = prefix;
+  const uint32_t need = remaining;
+
+  // ---- 2. counts above / equal to T before this thread's range (block scan)
+  uint32_t n_gt = 0u, n_eq = 0u;
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    n_gt += (j < n_valid && key[j] > T) ? 1u : 0u;
+    n_eq += (j < n_valid && key[j] == T) ? 1u : 0u;
+  }
+  uint32_t x_gt = n_gt, x_eq = n_eq;  // inclusive wave scans
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t a = __shfl_up(x_gt, off), b = __shfl_up(x_eq, off);
+    if (lane >= off) { x_gt += a; x_eq += b; }
+  }
+  if (lane == 63) { wsum_gt[wave] = x_gt; wsum_eq[wave] = x_eq; }
+  __syncthreads();
+  uint32_t gt_before = x_gt - n_gt, eq_before = x_eq - n_eq;
+  for (int w = 0; w < wave; ++w) { gt_before += wsum_gt[w]; eq_before += wsum_eq[w]; }
+
+  // ---- 3. this workgroup's share of output positions: its list in LDS
+  const int p0 = blockIdx.x * share, p1 = min(lp, p0 + share);
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    const bool gt = j < n_valid && key[j] > T;
+    const bool eq = j < n_valid && key[j] == T;
+    const uint32_t pos = gt_before + min(eq_before, need);
+    const bool sel = gt || (eq && eq_before < need);
+    if (sel && (int)pos >= p0 && (int)pos < p1) {
+      list_src[pos - p0] = i0 + j;
+      if (out_idx) out_idx[(size_t)head * lp + pos] = i0 + j;
+    }
+    gt_before += gt ? 1u : 0u;
+    eq_before += eq ? 1u : 0u;
+  }
+  __syncthreads();
+
+  // ---- 4. gather the share's rows with 16-byte copies
+  const int row_chunks = head_dim / 8;
+  const size_t M = (size_t)La + Lb;
+  const uint4* ksrc = reinterpret_cast<const uint4*>(k + (size_t)head * M * head_dim);
+  const uint4* vsrc = reinterpret_cast<const uint4*>(v + (size_t)head * M * head_dim);
+  uint4* kdst = reinterpret_cast<uint4*>(out_k + (size_t)head * lp * head_dim);
+  uint4* vdst = reinterpret_cast<uint4*>(out_v + (size_t)head * lp * head_dim);
+  const int pieces = (p1 - p0) * row_chunks;
+  for (int e = tid; e < 2 * pieces; e += kRegThreads) {
+    const int which = e >= pieces;  // 0: K, 1: V
+    const int ee = e - which * pieces;
+    const int r = ee / row_chunks, ch = ee - r * row_chunks;
+    const int li = list_src[r];
+    if (li < 0 || li >= Lb) continue;
+    const size_t src = ((size_t)La + li) * row_chunks + ch;
+    const size_t dst = (size_t)(p0 + r) * row_chunks + ch;
+    if (which) vdst[dst] = vsrc[src];
+    else kdst[dst] = ksrc[src];
+  }
+}
+
 }  // namespace
 
 hipError_t launch_compress(const CompressArgs& a, hipStream_t stream) {
   if (a.lp == 0) return hipSuccess;
+  if (a.Lb <= kRegThreads * 32) {
+    // a share of at most 1024 output rows per workgroup, about 64 rows each
+    // for the gather, at most 32 workgroups per head
+    int groups = (a.lp + 63) / 64;
+    groups = groups < 1 ? 1 : (groups > 32 ? 32 : groups);
+    int share = (a.lp + groups - 1) / groups;
+    if (share > 1024) {
+      share = 1024;
+      groups = (a.lp + share - 1) / share;
+    }
+    const dim3 grid(groups, a.n_kv);
+    if (a.Lb <= kRegThreads * 4)
+      hipLaunchKernelGGL(topk_gather_reg_kernel<4>, grid, dim3(kRegThreads), 0, stream, a.scores,
+                         a.k, a.v, a.idx, a.out_k, a.out_v, a.La, a.Lb, a.lp, a.head_dim, share);
+    else if (a.Lb <= kRegThreads * 16)
+      hipLaunchKernelGGL(topk_gather_reg_kernel<16>, grid, dim3(kRegThreads), 0, stream, a.scores,
+                         a.k, a.v, a.idx, a.out_k, a.out_v, a.La, a.Lb, a.lp, a.head_dim, share);
+    else
+      hipLaunchKernelGGL(topk_gather_reg_kernel<32>, grid, dim3(kRegThreads), 0, stream, a.scores,
+                         a.k, a.v, a.idx, a.out_k, a.out_v, a.La, a.Lb, a.lp, a.head_dim, share);
+    return hipGetLastError();
+  }
   // Enough workgroups per head to spread the gather over the chip, each
   // owning at least 1024 local indices.
   int splits = a.Lb / 1024;

@@ -231,6 +231,40 @@ def test_compress_edge_cases(case):
     _check_compress(p, inp, case)
 
 
+@pytest.mark.parametrize("case", ["misaligned_scores", "big_tie_groups"])
+def test_compress_layouts(case):
+    """Scores whose base is 4- but not 16-byte aligned (the vector loads step
+    aside), and a long local block of integer scores with selections of
+    thousands of rows per head (shares near the 1024-row limit)."""
+    torch = need_gpu()
+    from paper_2502_12085_amd import apb
+    rng = np.random.default_rng(7)
+    if case == "misaligned_scores":
+        lb, lp, d, n_kv, la = 5000, 1500, 128, 2, 16
+        s = rng.standard_normal((n_kv, lb)).astype(np.float32)
+    else:
+        lb, lp, d, n_kv, la = 30000, 29000, 64, 2, 0
+        s = rng.zipf(1.5, (n_kv, lb)).astype(np.float32)
+    p = inputs.Problem(4, 1, la, lb, lp, n_kv, n_kv, d)
+    k = rng.integers(0, 65536, (n_kv, la + lb, d), dtype=np.uint16)
+    v = rng.integers(0, 65536, (n_kv, la + lb, d), dtype=np.uint16)
+    flat = torch.zeros(n_kv * lb + 1, dtype=torch.float32, device="cuda")
+    ds = flat[1:].view(n_kv, lb)  # 4-byte aligned, never 16
+    ds.copy_(torch.from_numpy(s))
+    if case != "misaligned_scores":
+        ds = torch.from_numpy(s).cuda()
+    idx = torch.full((n_kv, lp), -1, dtype=torch.int32, device="cuda")
+    ok = torch.zeros((n_kv, lp, d), dtype=torch.bfloat16, device="cuda")
+    ov = torch.zeros_like(ok)
+    apb.compress_select(p, ds, dev_bf16(k), dev_bf16(v), idx, ok, ov)
+    torch.cuda.synchronize()
+    ridx, rk, rv = oracle.compress_ref(s, k, v, lp, la)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ridx)
+    np.testing.assert_array_equal(host_bits(ok), rk)
+    np.testing.assert_array_equal(host_bits(ov), rv)
+    say(f"  {case}: bit-exact")
+
+
 def test_simulated_hosts_end_to_end():
     """Alg. 2 on one GPU: every earlier host's compressor writes its slot of
     a rank-major passing buffer, then the last host's attention reads it."""
