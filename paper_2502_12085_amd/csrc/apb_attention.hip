@@ -18,24 +18,27 @@
 //    v_permlane32_swap, and the probabilities are already laid out as the B
 //    operand of O^T = V^T P^T: no LDS round trip for P.
 //  * Ping-pong: the waves form two groups of four (one wave of each per
-//    SIMD) that alternate between an MFMA phase (S of the next 64-key tile
+//    SIMD) that alternate between an MFMA phase (S of the next 128-key tile
 //    and the PV product of the previous one, interleaved) and a softmax
 //    phase, the phases separated by workgroup barriers.  On every SIMD one
 //    wave feeds the matrix core while the other runs its exp/FMA work; a
-//    single wave cannot overlap the two on gfx950.
-//  * K and V tiles (64 keys) are copied HBM -> LDS by global_load_lds_dwordx4
-//    (no register staging) into a 4-stage ring; the copies ride in the
-//    softmax phases (K by one group, V by the other) and are waited for just
-//    before the barrier that opens the phase reading them, 3-4 phases later.
+//    single wave cannot overlap the two on gfx950.  A phase carries a fixed
+//    cost (barrier, the first operand reads, the wait for the last MFMA
+//    results), so the tiles are as long as registers and LDS allow.
+//  * K and V tiles (128 keys) are copied HBM -> LDS by global_load_lds_dwordx4
+//    (no register staging) into two-stage rings: group B copies K at the
+//    start of its softmax phases, group A copies V at the start of its MFMA
+//    phases (interleaved with the matrix work), each with two phases to land.
 //  * LDS tiles are row-major with an XOR swizzle of their 16-byte chunks: the
 //    K operand reads (ds_read_b128) and the transposing V operand reads
 //    (ds_read_b64_tr_b16) are free of bank conflicts, and each read address
 //    is one XOR of a per-lane base plus an immediate.
 //  * Online softmax in fp32 registers in base 2 (scale*log2(e) folded into one
-//    FMA), probabilities rounded to bf16 for the PV product, fp32 accumulate.
-//    The running max moves lazily: probabilities are formed against the
-//    current max and the tile max is only computed when a tile's row sum
-//    exceeds 2^13, so the max pass and the O rescale are off the common path.
+//    FMA), probabilities rounded to bf16 for the PV product, fp32 accumulate,
+//    taken one 32-key block at a time (few live temporaries).  The running
+//    max moves lazily: probabilities are formed against the current max and
+//    the tile max is only computed when a tile's row sum exceeds 2^13, so
+//    the max pass and the O rescale are off the common path.
 //  * Tiles crossing a row's visible end are masked element-wise; tiles past
 //    every row of the workgroup are not visited.
 //  * Grid order puts the query tiles with the longest key prefix first, and
@@ -60,11 +63,10 @@ constexpr int kWaves = 2 * kGroupWaves;     // ping-pong groups A and B
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
 constexpr int kBM = kRowsPerWave * kWaves;  // query rows per workgroup
-constexpr int kBN = 64;                            // keys per tile
-constexpr int kStages = 4;                         // LDS ring depth for K and V tiles
-#ifndef APB_PD
-#define APB_PD 2
-#endif
+constexpr int kBN = 128;                           // keys per tile
+constexpr int kKB = kBN / 32;                      // 32-key blocks per tile
+constexpr int kStages = 2;                         // LDS ring depth for K and V tiles
+constexpr int kPD = 2;                             // LDS operand read-ahead (MFMA steps)
 constexpr int kXcds = 8;                    // MI355X: 8 XCDs, workgroups dealt round-robin
 constexpr float kSumLimit = 8192.f;         // lazy rescale: largest tile row-half sum against a stale max
 
@@ -170,11 +172,12 @@ attn_fwd_kernel(Params p) {
   constexpr int KCH = D / 8;                     // 16-byte chunks per key row
   constexpr int NKC = D / 16;                    // MFMA k-steps over head_dim
   constexpr int NDB = D / 32;                    // 32-wide blocks of head_dim in O^T
-  constexpr int NQK = 2 * NKC;                   // QK MFMAs per tile (two 32-key blocks)
-  constexpr int NPV = 4 * NDB;                   // PV MFMAs per tile (four 16-key steps)
-  constexpr int PD = APB_PD;                     // LDS operand prefetch depth (MFMA steps)
+  constexpr int NQK = kKB * NKC;                 // QK MFMAs per tile
+  constexpr int NPG = kBN / 16;                  // 16-key groups of P (PV k-steps)
+  constexpr int NPV = NPG * NDB;                 // PV MFMAs per tile
+  constexpr int PD = kPD;
   static_assert(PIECES * PIECE_ELEMS == kBN * D && WP * kGroupWaves == PIECES, "tile split");
-  static_assert(WP == 2 || WP == 4, "vmcnt immediates below");
+  static_assert(WP == 4 || WP == 8, "copy groups of four pieces");
   static_assert(NQK == NPV, "QK and PV step counts match for d in {64, 128}");
 
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kStages][kBN * D];
@@ -200,28 +203,33 @@ attn_fwd_kernel(Params p) {
   // MFMA step of tile t, {S(t) = K(t) Q^T, O += P(t-1) V(t-1)}, in phase 2t
   // and the softmax of S(t) in phase 2t+1; group B runs the same one phase
   // later, so on every SIMD one wave issues MFMAs while the other runs its
-  // exp/FMA work.  K(t) is read in phases 2t, 2t+1 and V(t) in 2t+2, 2t+3.
-  // The HBM -> LDS copies ride in the softmax phases: group B copies K(T) in
-  // phase 2T-4 and group A copies V(T) in phase 2T-3, both into ring stage
-  // T % kStages, whose previous tile was last read in phase 2T-5; each waits
-  // for its copy just before the barrier that opens the consuming phase.
+  // exp/FMA work.  K(t) is read in phases 2t and 2t+1, V(t) in 2t+2 and
+  // 2t+3.  Copies, into ring stage T % 2:
+  //  - group B copies K(T) at the start of phase 2T-2 (its softmax phase; the
+  //    stage's previous tile K(T-2) was last read in phase 2T-3) and waits
+  //    for it at the end of phase 2T-1 (its MFMA phase);
+  //  - group A copies V(T) at the start of phase 2T (its MFMA phase; V(T-2)
+  //    was last read in phase 2T-1) and waits for it at the end of phase
+  //    2T+1 (its softmax phase).
+  // The barrier after each wait makes the tile visible to the phase that
+  // first reads it.
 
   // Copy lanes: global_load_lds_dwordx4 puts lane l's 16 bytes at M0 +
   // inst_offset + 16*l and reads them from saddr + voffset + inst_offset, so
-  // one M0 serves the wave's WP pieces (1 KiB apart in LDS and, inside one
-  // segment, in HBM) and every lane fetches the chunk that belongs at its
+  // one M0 serves four of the wave's pieces (1 KiB apart in LDS and, inside
+  // one segment, in HBM) and every lane fetches the chunk that belongs at its
   // swizzled slot.  The copies are inline asm so the compiler does not order
   // the LDS operand reads behind them.
   const bool copies_v = grp == 0;
   const uint16_t* cp_loc = copies_v ? p.v : p.k;
   const uint16_t* cp_pass = copies_v ? p.vp : p.kp;
-  uint32_t cp_off[WP];  // per-lane byte offset of piece j, less j KiB
+  uint32_t cp_off[WP];  // per-lane byte offset of piece j, less (j % 4) KiB
 #pragma unroll
   for (int j = 0; j < WP; ++j) {
     const int row = (wig * WP + j) * ROWS_PER_PIECE + lane / KCH;
     const int slot = lane % KCH;
     const int swz = copies_v ? v_swz<D>(row) : k_swz<D>(row);
-    cp_off[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ swz)) - 1024u * j;
+    cp_off[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ swz)) - 1024u * (j % 4);
   }
   // Segment cursor: concatenated key rows c in [.., seg_end) sit at byte
   // address seg_base + 2*D*c.  Tiles are copied in increasing order, so the
@@ -248,23 +256,19 @@ attn_fwd_kernel(Params p) {
     if (c0 >= seg_end) seek(c0);
     uint16_t* stage = copies_v ? v_lds[T % kStages] : k_lds[T % kStages];
     if (c0 + kBN <= seg_end) {
-      const uint64_t base = uniform64(seg_base + (uint64_t)(2 * D) * (uint32_t)c0);
-      const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_offset(&stage[wig * WP * PIECE_ELEMS]));
-      if constexpr (WP == 4) {
+#pragma unroll
+      for (int g = 0; g < WP / 4; ++g) {
+        const uint64_t base = uniform64(seg_base + (uint64_t)(2 * D) * (uint32_t)c0);
+        const uint32_t dst = __builtin_amdgcn_readfirstlane(
+            lds_offset(&stage[(wig * WP + 4 * g) * PIECE_ELEMS]));
         asm volatile(
             "s_mov_b32 m0, %5\n\t"
             "global_load_lds_dwordx4 %0, %4\n\t"
             "global_load_lds_dwordx4 %1, %4 offset:1024\n\t"
             "global_load_lds_dwordx4 %2, %4 offset:2048\n\t"
-            "global_load_lds_dwordx4 %3, %4 offset:3072" ::"v"(cp_off[0]),
-            "v"(cp_off[1]), "v"(cp_off[2]), "v"(cp_off[3]), "s"(base), "s"(dst)
-            : "memory", "m0");
-      } else {
-        asm volatile(
-            "s_mov_b32 m0, %3\n\t"
-            "global_load_lds_dwordx4 %0, %2\n\t"
-            "global_load_lds_dwordx4 %1, %2 offset:1024" ::"v"(cp_off[0]),
-            "v"(cp_off[1]), "s"(base), "s"(dst)
+            "global_load_lds_dwordx4 %3, %4 offset:3072" ::"v"(cp_off[4 * g]),
+            "v"(cp_off[4 * g + 1]), "v"(cp_off[4 * g + 2]), "v"(cp_off[4 * g + 3]), "s"(base),
+            "s"(dst)
             : "memory", "m0");
       }
     } else {
@@ -283,19 +287,8 @@ attn_fwd_kernel(Params p) {
       }
     }
   };
-  // Wait until this wave's copies of tile T have landed, `later` of its
-  // copies of later tiles being allowed to stay in flight.
-  auto land = [&](int later) __attribute__((always_inline)) {
-    if (later >= 2) {
-      if constexpr (WP == 4) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    } else if (later == 1) {
-      if constexpr (WP == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
-  };
+  // Every wave has at most one tile's copies in flight when it waits.
+  auto land = []() __attribute__((always_inline)) { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
 
   const int w_first = r0 + kRowsPerWave * wave;
   const bool w_valid = w_first < p.M;
@@ -320,17 +313,18 @@ attn_fwd_kernel(Params p) {
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
-  f32x16 s[2];   // S^T of the current tile: two 32-key blocks
-  bf16x8 pb[4];  // P of the previous tile: four 16-key MFMA steps
+  f32x16 s[kKB];   // S^T of the current tile: one accumulator per 32-key block
+  bf16x8 pb[NPG];  // P of the previous tile: one MFMA B operand per 16-key group
   float m_run = -INFINITY;  // running max of scaled logits (base-2 units)
   float l_run = 0.f;        // this lane-half's share of the running sum
 
   // LDS operands, addressed as (stage base + lane base) ^ (step bits) +
   // immediate, so no per-step address registers stay live across tiles.
-  //  QK step i: k-step kc = i/2 over head_dim, key block i%2; the A operand
-  //  holds K rows (lane n holds key 32*(i%2) + n, chunk 2kc + h).  With the
-  //  K swizzle, chunk (2kc + h) of row n sits at byte 16*((h ^ n) & 1) +
-  //  16*(n & (KCH-2)) xor 32*kc of the row; the key block is the immediate.
+  //  QK step i: k-step kc = i / kKB over head_dim, key block i % kKB; the A
+  //  operand holds K rows (lane n holds key 32*(i%kKB) + n, chunk 2kc + h).
+  //  With the K swizzle, chunk (2kc + h) of row n sits at byte 16*((h ^ n) &
+  //  1) + 16*(n & (KCH-2)) xor 32*kc of the row; the key block is the
+  //  immediate.
   //  PV step i: 16-key group c = i / NDB, dim block db = i % NDB; pb[c] slot
   //  j of lane half hh holds key 16c + 8*(j/4) + 4*hh + j%4 (the S^T
   //  accumulator layout), and the A operand (dims x keys) comes from two
@@ -349,7 +343,7 @@ attn_fwd_kernel(Params p) {
                         8 * (sl & 1));
   }
   auto k_operand = [&](uint32_t kb, int i) -> bf16x8 __attribute__((always_inline)) {
-    const uint32_t a = (kb ^ (32u * (uint32_t)(i >> 1))) + (uint32_t)(64 * D * (i & 1));
+    const uint32_t a = (kb ^ (32u * (uint32_t)(i / kKB))) + (uint32_t)(64 * D * (i % kKB));
     return *(const lds_bf16x8*)(uintptr_t)a;
   };
   auto v_operand = [&](uint32_t vb, int i) -> bf16x8 __attribute__((always_inline)) {
@@ -367,59 +361,52 @@ attn_fwd_kernel(Params p) {
     oacc[i % NDB] =
         __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[i / NDB], oacc[i % NDB], 0, 0, 0);
   };
+  auto qk_step = [&](const bf16x8& a, int i) __attribute__((always_inline)) {
+    const f32x16 zero16 = {};
+    s[i % kKB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[i / kKB],
+                                                         i < kKB ? zero16 : s[i % kKB], 0, 0, 0);
+  };
 
   // MFMA steps.  qk_pv(t) computes S(t) = K(t) Q^T and O += P(t-1) V(t-1),
   // the two streams interleaved step by step with their LDS operands read PD
   // steps ahead into rotating registers; qk_only and pv_only are the first
-  // and last tiles.  The first PD steps' operands (kpre, vpre) are read at
-  // the end of the wave's preceding softmax phase, so an MFMA phase starts
-  // with its operands in registers.  The scheduling barriers keep the
-  // prefetch distance (the compiler would otherwise hoist every read of the
-  // tile and run out of registers).
+  // and last tiles.  The scheduling barriers keep the read-ahead distance
+  // (the compiler would otherwise hoist every read of the tile and run out
+  // of registers).
   auto k_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(k_lds[t % kStages]) + k_lane; };
   auto v_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(v_lds[t % kStages]) + v_lane; };
-  const f32x16 zero16 = {};
-  bf16x8 kpre[PD], vpre[PD];
-  auto pre_k = [&](int t) __attribute__((always_inline)) {
-    const uint32_t kl = k_stage(t);
-#pragma unroll
-    for (int i = 0; i < PD; ++i) kpre[i] = k_operand(kl, i);
-  };
-  auto pre_v = [&](int t) __attribute__((always_inline)) {
-    const uint32_t vl = v_stage(t);
-#pragma unroll
-    for (int i = 0; i < PD; ++i) vpre[i] = v_operand(vl, i);
-  };
-  auto qk_pv = [&](int t) __attribute__((always_inline)) {
+  // copy_v: group A's V(t) copies, issued behind the phase's first operand
+  // reads while the matrix core waits for them.
+  auto qk_pv = [&](int t, bool copy_v) __attribute__((always_inline)) {
     const uint32_t kl = k_stage(t), vl = v_stage(t - 1);
     bf16x8 ka[PD + 1], va[PD + 1];
 #pragma unroll
     for (int i = 0; i < PD; ++i) {
-      ka[i] = kpre[i];
-      va[i] = vpre[i];
+      ka[i] = k_operand(kl, i);
+      va[i] = v_operand(vl, i);
     }
+    if (copy_v) issue(t);
 #pragma unroll
     for (int i = 0; i < NQK; ++i) {
       if (i + PD < NQK) {
         ka[(i + PD) % (PD + 1)] = k_operand(kl, i + PD);
         va[(i + PD) % (PD + 1)] = v_operand(vl, i + PD);
       }
-      s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % (PD + 1)], qreg[i >> 1],
-                                                         i < 2 ? zero16 : s[i & 1], 0, 0, 0);
+      qk_step(ka[i % (PD + 1)], i);
       pv_step(va[i % (PD + 1)], i);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto qk_only = [&](int t) __attribute__((always_inline)) {
+  auto qk_only = [&](int t, bool copy_v) __attribute__((always_inline)) {
     const uint32_t kl = k_stage(t);
     bf16x8 ka[PD + 1];
 #pragma unroll
-    for (int i = 0; i < PD; ++i) ka[i] = kpre[i];
+    for (int i = 0; i < PD; ++i) ka[i] = k_operand(kl, i);
+    if (copy_v) issue(t);
 #pragma unroll
     for (int i = 0; i < NQK; ++i) {
       if (i + PD < NQK) ka[(i + PD) % (PD + 1)] = k_operand(kl, i + PD);
-      s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % (PD + 1)], qreg[i >> 1],
-                                                         i < 2 ? zero16 : s[i & 1], 0, 0, 0);
+      qk_step(ka[i % (PD + 1)], i);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -427,7 +414,7 @@ attn_fwd_kernel(Params p) {
     const uint32_t vl = v_stage(t);
     bf16x8 va[PD + 1];
 #pragma unroll
-    for (int i = 0; i < PD; ++i) va[i] = vpre[i];
+    for (int i = 0; i < PD; ++i) va[i] = v_operand(vl, i);
 #pragma unroll
     for (int i = 0; i < NPV; ++i) {
       if (i + PD < NPV) va[(i + PD) % (PD + 1)] = v_operand(vl, i + PD);
@@ -435,70 +422,66 @@ attn_fwd_kernel(Params p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // operands of the MFMA phase that follows softmax(t)
-  auto prefetch_after = [&](int t) __attribute__((always_inline)) {
-    if (t + 1 < ntiles) pre_k(t + 1);
-    pre_v(t);
-  };
 
   // Softmax of tile t: mask, running max, exp2, row sums, P -> bf16.
   auto softmax = [&](int t) __attribute__((always_inline)) {
     const int c0 = t * kBN;
     if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+      for (int b = 0; b < kKB; ++b)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int c = c0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (c >= rq_end) s[sb][r] = -INFINITY;
+          const int c = c0 + 32 * b + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (c >= rq_end) s[b][r] = -INFINITY;
         }
     }
     // Lazy running max without a max pass on the common path: the
     // probabilities are taken against the current (possibly stale) m_run,
     // and only when some row-half's tile sum exceeds kSumLimit (a logit far
     // above m_run, or the first tile, where m_run = -inf) does the wave find
-    // the tile max,
-    // move m_run up to it, rescale O and l, and redo the tile.  O and l
-    // share one m_run per row, and O / l and m_run*ln2 + ln(l) do not depend
-    // on its value.
-    // The tile is processed in three batches (all FMAs, all exp2, then the
-    // sums and bf16 packing) so that no instruction waits on the latency of
-    // the one before it: a lone wave issues VALU work slowly enough already.
-    float rs[8];
+    // the tile max, move m_run up to it, rescale O and l, and redo the tile.
+    // O and l share one m_run per row, and O / l and m_run*ln2 + ln(l) do
+    // not depend on its value.
+    // Each 32-key block is processed in three batches (its FMAs, its exp2,
+    // then its sums and bf16 packing) so that no instruction waits on the
+    // latency of the one before it, and only one block's exponentials are
+    // live at a time.
+    float rs[4];
     auto exp_tile = [&]() __attribute__((always_inline)) {
-      f32x16 e[2];
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+      for (int j = 0; j < 4; ++j) rs[j] = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) e[sb][r] = fmaf(s[sb][r], p.scale_log2, -m_run);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int b = 0; b < kKB; ++b) {
+        f32x16 e;
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+        for (int r = 0; r < 16; ++r) e[r] = fmaf(s[b][r], p.scale_log2, -m_run);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) e[sb][r] = __builtin_amdgcn_exp2f(e[sb][r]);
-      __builtin_amdgcn_sched_barrier(0);
-      // eight independent sum chains, chain j over elements 4j .. 4j+3
+        for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(e[r]);
+        __builtin_amdgcn_sched_barrier(0);
+        // four independent sum chains, chain j over elements 4j .. 4j+3
 #pragma unroll
-      for (int j = 0; j < 8; ++j) rs[j] = e[j >> 2][4 * (j & 3)];
+        for (int k = 0; k < 4; ++k)
 #pragma unroll
-      for (int k = 1; k < 4; ++k)
+          for (int j = 0; j < 4; ++j) rs[j] += e[4 * j + k];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) rs[j] += e[j >> 2][4 * (j & 3) + k];
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e[sb][r];
+        for (int r = 0; r < 16; ++r) pb[2 * b + (r >> 3)][r & 7] = (__bf16)e[r];
+      }
     };
     exp_tile();
-    const float l_tile = ((rs[0] + rs[1]) + (rs[2] + rs[3])) + ((rs[4] + rs[5]) + (rs[6] + rs[7]));
+    const float l_tile = (rs[0] + rs[1]) + (rs[2] + rs[3]);
     if (__any(!(l_tile <= kSumLimit))) {
       float mq[4];  // four independent max chains
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j >> 1][8 * (j & 1)], s[j >> 1][8 * (j & 1) + 1]);
+      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j][0], s[j][1]);
 #pragma unroll
-      for (int r = 2; r < 8; ++r)
+      for (int r = 2; r < 16; ++r)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j >> 1][8 * (j & 1) + r]);
+        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j % kKB][r]);
+#pragma unroll
+      for (int b = 4; b < kKB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mq[r & 3] = fmaxf(mq[r & 3], s[b][r]);
       float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
       mx = fmaxf(mx, half_swap(mx));
       const float m_new = fmaxf(m_run, mx * p.scale_log2);
@@ -511,7 +494,7 @@ attn_fwd_kernel(Params p) {
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
       exp_tile();
     }
-    l_run += ((rs[0] + rs[1]) + (rs[2] + rs[3])) + ((rs[4] + rs[5]) + (rs[6] + rs[7]));
+    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
   };
 
   // Tiles a wave's rows cannot see need no branch: the mask sets their
@@ -519,76 +502,60 @@ attn_fwd_kernel(Params p) {
   // not move.  The MFMA priority lets the MFMA wave win issue arbitration
   // over the softmax wave sharing its SIMD.
   auto mfma_prio = []() __attribute__((always_inline)) { __builtin_amdgcn_s_setprio(1); };
-  auto vmem_prio = []() __attribute__((always_inline)) { __builtin_amdgcn_s_setprio(0); };
-  // Copy schedule: group B copies K(T) in phase 2T-4 and waits for it at the
-  // end of phase 2T-2; group A copies V(T) in phase 2T-3 and waits for it at
-  // the end of phase 2T-1.  The barrier after each wait makes the tile
-  // visible to the prefetch at the end of the phase before its first MFMA
-  // phase.  Ring stage T % 4 is rewritten only after its previous tile's last
-  // reader (phase 2T-7 for K, 2T-5 for V).
+  auto base_prio = []() __attribute__((always_inline)) { __builtin_amdgcn_s_setprio(0); };
+  // Both groups pass the same number of barriers: one after the prologue,
+  // then two per tile, then two for the last PV products.
   if (grp == 0) {
     // group A: copies V; MFMA(t) in phase 2t, softmax(t) in phase 2t+1
-    issue(0);
-    if (ntiles > 1) issue(1);
-    land(ntiles > 1 ? 1 : 0);  // V(0)
-    phase_barrier();
-    pre_k(0);
+    phase_barrier();  // K(0) landed (copied by group B)
     mfma_prio();
-    qk_only(0);
-    vmem_prio();
+    qk_only(0, true);
+    base_prio();
     phase_barrier();
-    auto a_softmax_phase = [&](int t) __attribute__((always_inline)) {
-      if (t + 2 < ntiles) issue(t + 2);
-      softmax(t);
-      prefetch_after(t);
-      if (t + 1 < ntiles) land(t + 2 < ntiles ? 1 : 0);  // V(t+1)
-      phase_barrier();
-    };
-    a_softmax_phase(0);
+    softmax(0);
+    land();  // V(0)
+    phase_barrier();
     for (int t = 1; t < ntiles; ++t) {
       mfma_prio();
-      qk_pv(t);
-      vmem_prio();
+      qk_pv(t, true);
+      base_prio();
       phase_barrier();
-      a_softmax_phase(t);
+      softmax(t);
+      land();  // V(t)
+      phase_barrier();
     }
     mfma_prio();
     pv_only(ntiles - 1);
-    vmem_prio();
+    base_prio();
     phase_barrier();
     phase_barrier();
   } else {
     // group B: copies K; MFMA(t) in phase 2t+1, softmax(t) in phase 2t+2
     issue(0);
-    if (ntiles > 1) issue(1);
-    land(ntiles > 1 ? 1 : 0);  // K(0)
+    land();  // K(0)
     phase_barrier();
-    if (2 < ntiles) issue(2);
-    pre_k(0);
-    if (1 < ntiles) land(2 < ntiles ? 1 : 0);  // K(1)
+    if (1 < ntiles) issue(1);
     phase_barrier();
-    auto b_softmax_phase = [&](int t) __attribute__((always_inline)) {
-      if (t + 3 < ntiles) issue(t + 3);
-      softmax(t);
-      prefetch_after(t);
-      if (t + 2 < ntiles) land(t + 3 < ntiles ? 1 : 0);  // K(t+2)
-      phase_barrier();
-    };
     mfma_prio();
-    qk_only(0);
-    vmem_prio();
+    qk_only(0, false);
+    base_prio();
+    land();  // K(1)
     phase_barrier();
-    b_softmax_phase(0);
     for (int t = 1; t < ntiles; ++t) {
-      mfma_prio();
-      qk_pv(t);
-      vmem_prio();
+      if (t + 1 < ntiles) issue(t + 1);
+      softmax(t - 1);
       phase_barrier();
-      b_softmax_phase(t);
+      mfma_prio();
+      qk_pv(t, false);
+      base_prio();
+      land();  // K(t+1)
+      phase_barrier();
     }
+    softmax(ntiles - 1);
+    phase_barrier();
     mfma_prio();
     pv_only(ntiles - 1);
-    vmem_prio();
+    base_prio();
     phase_barrier();
   }
 
