@@ -44,8 +44,8 @@ typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
 constexpr int kRows = 32;   // rows per workgroup (the MFMA N side)
 constexpr int kKeys = 32;   // keys per block (the MFMA M side)
+constexpr int kWgPerCu = 3; // one-wave workgroups per CU (LDS: 3 x 48 KiB at d = 128)
 constexpr int kRing = 3;    // LDS stages of K and V blocks per workgroup
-constexpr int kWgPerCu = 3; // workgroups per CU (LDS: 3 x 48 KiB at d = 128)
 constexpr float kSumLimit = 8192.f;  // lazy rescale: largest block row-half sum against a stale max
 
 struct DecParams {
@@ -76,6 +76,25 @@ __device__ __forceinline__ int v_swz(int r) { return (4 * (r & 3)) & (D / 8 - 1)
 
 __device__ __forceinline__ uint32_t lds_offset(const uint16_t* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint16_t*)p;
+}
+
+// s_waitcnt vmcnt(N) for a compile-time N (at most 63).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait until at most `later` (0 <= later <= MAXN) blocks of CPW copies each
+// are outstanding.
+template <int CPW, int MAXN>
+__device__ __forceinline__ void wait_blocks(int later) {
+  if constexpr (MAXN > 0) {
+    if (later < MAXN) {
+      wait_blocks<CPW, MAXN - 1>(later);
+      return;
+    }
+  }
+  wait_vmcnt<CPW * MAXN>();
 }
 
 // Key / value row c of the concatenation [cache; new] of KV head kvh.
@@ -249,26 +268,21 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
   float m_run = -INFINITY, l_run = 0.f;
 
   // three-stage ring: blocks b+1 and b+2 fly while block b is computed
-  if (b0 < b1) load_block(b0, 0);
-  if (b0 + 1 < b1) load_block(b0 + 1, 1);
+  // (a deeper ring for the eight-wave workgroups measured slower)
+#pragma unroll
+  for (int i = 0; i < kRing - 1; ++i)
+    if (b0 + i < b1) load_block(b0 + i, i);
+  static_assert(CPW * (kRing - 2) <= 63, "vmcnt immediate range");
   for (int b = b0; b < b1; ++b) {
     const int buf = (b - b0) % kRing;
-    // block b has landed once at most block b+1's copies are outstanding
-    // (with one wave its own wait suffices, with W the barrier below); then block b+2
-    // goes into the stage block b-1 used, whose reads ended with the
-    // previous iteration
-    if (b + 1 < b1) {
-      if constexpr (CPW == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-      else if constexpr (CPW == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-      else if constexpr (CPW == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(1)" ::: "memory");
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
+    // block b has landed once only the blocks issued after it are
+    // outstanding (with one wave its own wait suffices, with W the barrier
+    // below makes every wave's share visible)
+    wait_blocks<CPW, kRing - 2>(min(b1 - 1 - b, kRing - 2));
     // every wave's copies of block b have landed, and every wave is done
-    // with block b-1, whose stage block b+2 reuses
+    // with block b-1, whose stage block b+kRing-1 reuses
     if constexpr (W > 1) asm volatile("s_barrier" ::: "memory");
-    if (b + 2 < b1) load_block(b + 2, (b - b0 + 2) % kRing);
+    if (b + kRing - 1 < b1) load_block(b + kRing - 1, (b - b0 + kRing - 1) % kRing);
     const uint32_t kl = lds_offset(k_lds[buf]);
     bf16x8 kop[NKC];
 #pragma unroll
@@ -370,31 +384,35 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
 
 // MergeScore over n_parts partial results of `rows` rows: one workgroup per
 // row.  The d/4 threads of a group cover the row's d outputs (four each) and
-// the 256/(d/4) groups split the parts among themselves, so both many parts
-// (the splits of one decode call) and few parts with many rows (the hosts of
-// a decoding step) keep loads in flight; the groups' sums meet in LDS.
-template <typename OutT>
-__global__ void __launch_bounds__(256) merge_kernel(int n_parts, int rows, int d,
-                                                    const float* __restrict__ o_parts,
-                                                    const float* __restrict__ lse_parts,
-                                                    OutT* __restrict__ o, float* __restrict__ lse) {
-  __shared__ float red[8];
-  __shared__ __attribute__((aligned(16))) float acc_lds[256 * 4];
-  __shared__ float tot_lds[64];
+// the THREADS/(d/4) groups split the parts among themselves, so both many
+// parts (the splits of one decode call) and few parts with many rows (the
+// hosts of a decoding step) keep loads in flight; the groups' sums meet in
+// LDS.  THREADS = 1024 when there are few rows and many parts.
+template <typename OutT, int THREADS>
+__global__ void __launch_bounds__(THREADS) merge_kernel(int n_parts, int rows, int d,
+                                                        const float* __restrict__ o_parts,
+                                                        const float* __restrict__ lse_parts,
+                                                        OutT* __restrict__ o, float* __restrict__ lse) {
+  constexpr int NW = THREADS / 64;
+  __shared__ float red[NW];
+  __shared__ __attribute__((aligned(16))) float acc_lds[THREADS * 4];
+  __shared__ float tot_lds[THREADS / 16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = blockIdx.x;
-  const int tpr = d / 4, G = 256 / tpr;
+  const int tpr = d / 4, G = THREADS / tpr;
   const int grp = tid / tpr, c = (tid % tpr) * 4;
   const float* lrow = lse_parts + row;
 
   // 1. m = max over the parts' lse
   float m = -INFINITY;
-  for (int q = tid; q < n_parts; q += 256) m = fmaxf(m, lrow[(size_t)q * rows]);
+  for (int q = tid; q < n_parts; q += THREADS) m = fmaxf(m, lrow[(size_t)q * rows]);
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
   if (lane == 0) red[wave] = m;
   __syncthreads();
-  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  m = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) m = fmaxf(m, red[w]);
 
   // 2. this group's parts, four loads in flight per thread
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -448,8 +466,15 @@ template <typename OutT>
 hipError_t launch_merge_t(int n_parts, int rows, int d, const float* o_parts,
                           const float* lse_parts, OutT* o, float* lse, hipStream_t stream) {
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(merge_kernel<OutT>, dim3((unsigned)rows), dim3(256), 0, stream, n_parts, rows,
-                     d, o_parts, lse_parts, o, lse);
+  // few rows, many parts (the key splits of one generated token): spread
+  // each row's parts over 1024 threads so every thread has few loads to wait
+  // for; otherwise 256 threads per row
+  if (rows < 256 && n_parts >= 16)
+    hipLaunchKernelGGL((merge_kernel<OutT, 1024>), dim3((unsigned)rows), dim3(1024), 0, stream,
+                       n_parts, rows, d, o_parts, lse_parts, o, lse);
+  else
+    hipLaunchKernelGGL((merge_kernel<OutT, 256>), dim3((unsigned)rows), dim3(256), 0, stream,
+                       n_parts, rows, d, o_parts, lse_parts, o, lse);
   return hipGetLastError();
 }
 

@@ -10,10 +10,16 @@
 // (tokens t, output features f, weights row-major [f][k]).  One kernel
 // template covers them: bf16 MFMA 32x32x16 with fp32 accumulation, output
 // features on the MFMA M side (the weights are the A operand) and tokens on
-// the N side, a 256 x 256 workgroup tile of 8 waves (2 x 4, each 128
-// features x 64 tokens), K steps of 64 whose weight and token slabs are
-// copied HBM -> LDS by global_load_lds_dwordx4 into XOR-swizzled tiles (two
-// stages: the next step's copies fly while the current one is multiplied).
+// the N side, a 256 x 256 workgroup tile of 4 waves (2 x 2, each 128
+// features x 128 tokens, one wave per SIMD, accumulators in AGPRs), K steps
+// of 64 whose weight and token slabs are copied HBM -> LDS by
+// global_load_lds_dwordx4 into XOR-swizzled tiles in two stages.  The step
+// boundary is software-pipelined: at its last 16-deep substep a wave waits
+// for its copies of the next step, passes the barrier, and issues that
+// substep's MFMAs with the next step's first operand reads and the copies of
+// the step after it (into the stage just finished) behind them; the last two
+// steps are peeled so the steady-state loop has no branches (the compiler
+// can then count outstanding LDS reads exactly).
 // The token operand is read either row-major [t][k] or head-major
 // [k / dh][t][dh] (the attention output, whose heads are the O projection's
 // K dimension), so no transpose is ever materialised.  Epilogues:
@@ -24,6 +30,8 @@
 //    rows of the same features, so gate and up of one feature sit in the
 //    same lane and register slot and SiLU(gate) * up is formed in registers.
 #include <math.h>
+
+#include <type_traits>
 
 #include "apb_internal.h"
 
@@ -39,7 +47,8 @@ typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 constexpr int kBF = 256;        // weight rows (output features) per workgroup
 constexpr int kBT = 256;        // tokens per workgroup
 constexpr int kBK = 64;         // K per step
-constexpr int kGemmThreads = 512;
+constexpr int kGemmThreads = 256;
+constexpr int kPieces = 8;      // 1 KiB copy pieces per slab per wave per step
 constexpr int kTileElems = kBF * kBK;  // = kBT * kBK
 
 enum XMode { kXRowMajor = 0, kXHeadMajor = 1 };
@@ -63,9 +72,10 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
 }
 
-// 16-byte chunk c of tile row r sits at chunk c ^ (r & 7): the 8 rows one
-// ds_read_b128 pass touches hit 8 different chunk slots.
-__device__ __forceinline__ int swz(int r) { return r & 7; }
+// 16-byte chunk c of tile row r (128 bytes) sits at chunk c ^ ((r >> 1) & 7):
+// any 16 consecutive rows, which one 16-lane pass of ds_read_b128 touches,
+// land on 16 distinct 16-byte slots of the 256 bank bytes.
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 template <int XM, int WM, int EPI>
 __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
@@ -74,22 +84,22 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave & 1, wn = wave >> 1;  // feature half, token quarter
+  const int wm = wave & 1, wn = wave >> 1;  // feature half, token half
   const int n = lane & 31, h = lane >> 5;
   const int t0 = blockIdx.x * kBT;
   const int f0 = blockIdx.y * (WM == kWGateUp ? kBF / 2 : kBF);
   const int nk = p.K / kBK;
 
   // ---- copies: piece j (8 rows x 128 bytes) of each slab; wave w copies
-  // pieces 4w .. 4w+3.  Lane l takes row l/8 of the piece and fetches the
+  // pieces 8w .. 8w+7.  Lane l takes row l/8 of the piece and fetches the
   // chunk that belongs at slot l%8.  Rows past the last feature or token
   // repeat it (their results are never stored).
   const int cp_row = lane >> 3, cp_slot = lane & 7;
-  const uint16_t* w_src[4];
-  const uint16_t* x_src[4];
+  const uint16_t* w_src[kPieces];
+  const uint16_t* x_src[kPieces];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rho = 8 * (4 * wave + i) + cp_row;  // slab row 0..255
+  for (int i = 0; i < kPieces; ++i) {
+    const int rho = 8 * (kPieces * wave + i) + cp_row;  // slab row 0..255
     const int chunk = 8 * (cp_slot ^ swz(rho));
     int fr;
     const uint16_t* wm_base = p.w;
@@ -108,20 +118,22 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
     else
       x_src[i] = p.x + (size_t)tr * p.K + chunk;
   }
-  auto issue = [&](int kk, int st) __attribute__((always_inline)) {
+  // copy q (0..15) of step kk into stage st: q < 8 weight pieces, else token pieces
+  auto copy = [&](int kk, int st, int q) __attribute__((always_inline)) {
     const int k0 = kk * kBK;
-    size_t xoff = (size_t)k0;
-    if constexpr (XM == kXHeadMajor) xoff = (size_t)(k0 / p.dh) * p.T * p.dh + (k0 % p.dh);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int j = 4 * wave + i;
-      const uint32_t wd = __builtin_amdgcn_readfirstlane(lds_offset(&a_lds[st][j * 512]));
-      const uint32_t xd = __builtin_amdgcn_readfirstlane(lds_offset(&b_lds[st][j * 512]));
+    const int i = q & 7;
+    const int j = kPieces * wave + i;
+    if (q < 8) {
+      const uint32_t d = __builtin_amdgcn_readfirstlane(lds_offset(&a_lds[st][j * 512]));
       asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(w_src[i] + k0),
-                   "s"(wd)
+                   "s"(d)
                    : "memory", "m0");
+    } else {
+      size_t xoff = (size_t)k0;
+      if constexpr (XM == kXHeadMajor) xoff = (size_t)(k0 / p.dh) * p.T * p.dh + (k0 % p.dh);
+      const uint32_t d = __builtin_amdgcn_readfirstlane(lds_offset(&b_lds[st][j * 512]));
       asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(x_src[i] + xoff),
-                   "s"(xd)
+                   "s"(d)
                    : "memory", "m0");
     }
   };
@@ -134,56 +146,80 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
                                             16 * ((2 * kc + h) ^ swz(row)));
   };
   auto b_read = [&](int st, int nb, int kc) __attribute__((always_inline)) -> bf16x8 {
-    const int row = 64 * wn + 32 * nb + n;
+    const int row = 128 * wn + 32 * nb + n;
     return *(const lds_bf16x8*)(uintptr_t)(lds_offset(b_lds[st]) + row * 128 +
                                             16 * ((2 * kc + h) ^ swz(row)));
   };
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
+  bf16x8 av[2][4], bv[2][4];
 
-  issue(0, 0);
-  for (int kk = 0; kk < nk; ++kk) {
+  // prologue: step 0 copied and visible, step 1's copies in flight, step 0's
+  // first operands read
+#pragma unroll
+  for (int q = 0; q < 16; ++q) copy(0, 0, q);
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  if (nk > 1) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) copy(1, 1, q);
+  }
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) av[0][mb] = a_read(0, mb, 0);
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) bv[0][nb] = b_read(0, nb, 0);
+
+  // One K step in four substeps of 16 MFMAs, each followed by the next
+  // substep's eight operand reads.  NEXT: step kk+1 exists (at the last
+  // substep: wait for its copies, barrier, read its first operands); COPY:
+  // step kk+2 exists (its copies, into the stage this step used).
+  auto step = [&](int kk, auto next_t, auto copy_t) __attribute__((always_inline)) {
+    constexpr bool NEXT = decltype(next_t)::value, COPY = decltype(copy_t)::value;
     const int st = kk & 1;
-    // this wave's copies of step kk have landed; after the barrier every
-    // wave's have, and every wave is done reading the other stage
-    asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (kk + 1 < nk) issue(kk + 1, st ^ 1);
-    bf16x8 av[2][4], bv[2][2];
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) av[0][mb] = a_read(st, mb, 0);
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) bv[0][nb] = b_read(st, nb, 0);
 #pragma unroll
     for (int kc = 0; kc < 4; ++kc) {
-      const int cur = kc & 1;
-      if (kc + 1 < 4) {
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) av[cur ^ 1][mb] = a_read(st, mb, kc + 1);
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) bv[cur ^ 1][nb] = b_read(st, nb, kc + 1);
+      const int cur = kc & 1, nxt = cur ^ 1;
+      const bool boundary = kc == 3;
+      if (boundary && NEXT) {
+        // this wave's copies of step kk+1 have landed and its reads of stage
+        // st are done; after the barrier every wave's are
+        asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
       }
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[cur][mb], bv[cur][nb],
-                                                                acc[mb][nb], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int i = 0; i < 16; ++i) {
+        const int mb = i >> 2, nb = i & 3;
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[cur][mb], bv[cur][nb],
+                                                              acc[mb][nb], 0, 0, 0);
+        if (!boundary) {
+          if (i < 4) av[nxt][i] = a_read(st, i, kc + 1);
+          else if (i < 8) bv[nxt][i - 4] = b_read(st, i - 4, kc + 1);
+        } else if (NEXT) {
+          if (i < 4) av[nxt][i] = a_read(st ^ 1, i, 0);
+          else if (i < 8) bv[nxt][i - 4] = b_read(st ^ 1, i - 4, 0);
+          if (COPY) copy(kk + 2, st, i);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-  }
+  };
+  const std::true_type yes{};
+  const std::false_type no{};
+  int kk = 0;
+  for (; kk + 2 < nk; ++kk) step(kk, yes, yes);
+  if (kk + 1 < nk) step(kk++, yes, no);
+  step(kk, no, no);
 
   // ---- epilogue.  Lane (n, h), block (mb, nb), element r holds slab row
-  // 128*wm + 32*mb + 8*(r/4) + 4*h + r%4 of token t0 + 64*wn + 32*nb + n;
+  // 128*wm + 32*mb + 8*(r/4) + 4*h + r%4 of token t0 + 128*wn + 32*nb + n;
   // each group of four r is four consecutive features (one 8-byte store).
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int t = t0 + 64 * wn + 32 * nb + n;
+  for (int nb = 0; nb < 4; ++nb) {
+    const int t = t0 + 128 * wn + 32 * nb + n;
     if (t >= p.T) continue;
     if constexpr (EPI == kEpiSwiglu) {
 #pragma unroll

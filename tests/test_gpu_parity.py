@@ -150,9 +150,16 @@ def test_llama8b_32k_heads_subset_full_rows():
     _full_check(_wl("llama8b_32k"), heads=np.array([0, 5, 10, 15, 16, 22, 27, 31]))
 
 
+def test_d64_many_tiles_full_rows():
+    """head_dim 64 over many key and query tiles (26 key tiles of 128, ten
+    query tiles, GQA 4, a ragged passing block), every row of every head."""
+    _full_check(inputs.Workload("d64_mid", inputs.Problem(4, 3, 512, 2048, 250, 8, 2, 64)))
+
+
 def _sample_rows(p, rng, n_random=24):
     M = p.rows
-    fixed = {0, 1, 63, 64, 127, 128, p.anchor_len - 1, p.anchor_len, p.anchor_len + 1,
+    fixed = {0, 1, 63, 64, 127, 128, 255, 256, 511, 512, p.anchor_len - 1, p.anchor_len,
+             p.anchor_len + 1,
              p.anchor_len + 127, p.anchor_len + 128, M - 129, M - 128, M - 2, M - 1}
     fixed = {r for r in fixed if 0 <= r < M}
     return np.array(sorted(fixed | set(rng.integers(0, M, n_random).tolist())))
