@@ -283,15 +283,37 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
     // with block b-1, whose stage block b+kRing-1 reuses
     if constexpr (W > 1) asm volatile("s_barrier" ::: "memory");
     if (b + kRing - 1 < b1) load_block(b + kRing - 1, (b - b0 + kRing - 1) % kRing);
+    // All operand reads of a block are issued ahead of the MFMAs that use
+    // them (the scheduling barriers stop the compiler from re-serialising
+    // read, wait, MFMA): the K operands, then the QK MFMAs, then the V
+    // operands, which land while the softmax runs.
     const uint32_t kl = lds_offset(k_lds[buf]);
     bf16x8 kop[NKC];
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc)
       kop[kc] = *(const lds_bf16x8*)(uintptr_t)(kl + (k_lane ^ (32u * (uint32_t)kc)));
+    __builtin_amdgcn_sched_barrier(0);
     f32x16 s = {};
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc)
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qreg[kc], s, 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    const uint32_t vb = lds_offset(v_lds[buf]);
+    bf16x8 vop[2][NDB];
+#pragma unroll
+    for (int cst = 0; cst < 2; ++cst)
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const uint32_t x = vb + (v_lane ^ (64u * (uint32_t)db));
+        i16x4 part[2];
+#pragma unroll
+        for (int rd = 0; rd < 2; ++rd)
+          part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(uintptr_t)(x + (uint32_t)((16 * cst + 8 * rd) * 2 * D)));
+        vop[cst][db] = __builtin_bit_cast(
+            bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+    __builtin_amdgcn_sched_barrier(0);
     // mask: element r of this lane is key b*32 + 8*(r/4) + 4*h + r%4 of row
     // rho; only blocks that reach past the cache can hide keys
     const int c0 = b * kKeys;
@@ -344,22 +366,13 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
       }
     }
     l_run += rs;
-    // O^T += V^T P^T: the V tile of block b is in LDS (waited for above)
-    const uint32_t vb = lds_offset(v_lds[buf]);
+    // O^T += V^T P^T with the V operands read above
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int cst = 0; cst < 2; ++cst)
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const uint32_t x = vb + (v_lane ^ (64u * (uint32_t)db));
-        i16x4 part[2];
-#pragma unroll
-        for (int rd = 0; rd < 2; ++rd)
-          part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4*)(uintptr_t)(x + (uint32_t)((16 * cst + 8 * rd) * 2 * D)));
-        const bf16x8 a = __builtin_bit_cast(
-            bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[cst], oacc[db], 0, 0, 0);
-      }
+      for (int db = 0; db < NDB; ++db)
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[cst][db], pb[cst], oacc[db], 0, 0, 0);
     // every lane's LDS reads of this buffer are done before it is refilled
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   }
