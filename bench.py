@@ -62,6 +62,25 @@ def _oracle_threads() -> int:
         return os.cpu_count() or 1
 
 
+def host_info() -> dict:
+    """The host the oracle runs on: CPU model and the cores this process may
+    use (the container's share, not the machine's)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        nproc = os.cpu_count() or 1
+    return {"cpu_model": model, "nproc": nproc}
+
+
 def cpu_baseline(wl, inp, budget_s: float):
     """fp64 oracle on a bounded sample: whole query heads (all rows), as many
     as fit the time budget (at least one)."""
@@ -84,7 +103,7 @@ def cpu_baseline(wl, inp, budget_s: float):
             "cores": int(cores), "kind": "oracle",
             "sample": f"{heads} of {p.n_q_heads} query heads, all {p.rows} rows, fp64 NumPy; "
                       f"{el:.1f} s wall",
-            "seconds": round(el, 3)}
+            "seconds": round(el, 3), **host_info()}
 
 
 def busy_ahead(stream, ms: float = 20.0) -> None:

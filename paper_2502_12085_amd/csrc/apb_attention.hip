@@ -27,8 +27,8 @@
 //    results), so the tiles are as long as registers and LDS allow.
 //  * K and V tiles (128 keys) are copied HBM -> LDS by global_load_lds_dwordx4
 //    (no register staging) into two-stage rings: group B copies K at the
-//    start of its softmax phases, group A copies V at the start of its MFMA
-//    phases (interleaved with the matrix work), each with two phases to land.
+//    start of its softmax phases, group A copies V early in its MFMA phases
+//    (behind the phase's first operand reads), each with two phases to land.
 //  * LDS tiles are row-major with an XOR swizzle of their 16-byte chunks: the
 //    K operand reads (ds_read_b128) and the transposing V operand reads
 //    (ds_read_b64_tr_b16) are free of bank conflicts, and each read address
