@@ -43,7 +43,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
 constexpr int kRows = 32;   // rows per workgroup (the MFMA N side)
-constexpr int kKeys = 32;   // keys per block (the MFMA M side)
+constexpr int kKeys = 32;   // keys per MFMA block (the MFMA M side)
 constexpr int kWgPerCu = 3; // one-wave workgroups per CU (LDS: 3 x 48 KiB at d = 128)
 constexpr int kRing = 3;    // LDS stages of K and V blocks per workgroup
 constexpr float kSumLimit = 8192.f;  // lazy rescale: largest block row-half sum against a stale max
@@ -109,16 +109,25 @@ __device__ __forceinline__ const uint16_t* kv_row(const DecParams& p, const uint
 // W * blockIdx.z + w.  W = 1 for few rows (one generated token); W = 8 when a
 // GQA group has many rows (the question tokens), so that each K/V block is
 // copied once for 256 rows instead of once per 32.
+// Keys per ring block: one 32-key MFMA block for a one-wave workgroup
+// (three of them share a CU's LDS); two when eight waves share the ring, so
+// the block's wait and barrier are paid once per 64 keys and its QK products
+// run as two independent accumulator chains.
+template <int W>
+constexpr int block_keys() { return W == 1 ? kKeys : 2 * kKeys; }
+
 template <int D, int W>
 __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
+  constexpr int KB = block_keys<W>() / kKeys;  // 32-key MFMA blocks per ring block
+  constexpr int BK = KB * kKeys;             // keys per ring block
   constexpr int NKC = D / 16;                // MFMA k-steps over head_dim
   constexpr int NDB = D / 32;                // 32-dim blocks of O^T
   constexpr int KCH = D / 8;                 // 16-byte chunks per row
-  constexpr int PIECES = kKeys * D / 512;    // 1 KiB copies per K or V tile
-  static_assert(PIECES == 4 || PIECES == 8, "copy unrolling below");
+  constexpr int PIECES = BK * D / 512;       // 1 KiB copies per K or V tile
+  static_assert(W > 1 || PIECES == 4 || PIECES == 8, "copy unrolling below");
   constexpr int ROWS_PER_PIECE = 512 / D;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kRing][kKeys * D];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kRing][kKeys * D];
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kRing][BK * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kRing][BK * D];
 
   const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
   const int wave = W == 1 ? 0 : __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -128,7 +137,7 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
   constexpr int CPW = 2 * PIECES / W;
   static_assert(CPW * W == 2 * PIECES && CPW >= 1, "pieces split evenly over the waves");
   const int Ltot = p.Lc + (p.append ? p.n_new : 0);
-  const int nblk = (Ltot + kKeys - 1) / kKeys;
+  const int nblk = (Ltot + BK - 1) / BK;
   const int b0 = split * p.blocks_per_split;
   const int b1 = min(b0 + p.blocks_per_split, nblk);
 
@@ -183,9 +192,9 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
   // W > 1: this wave's copies, piece q = wave + W*i of the 2*PIECES pieces
   // (K pieces first, then V): one scalar base and one M0 per piece
   auto load_share = [&](int b, int buf) __attribute__((always_inline)) {
-    const int c0 = b * kKeys;
-    const bool in_cache = c0 + kKeys <= p.Lc;
-    const bool in_new = c0 >= p.Lc && c0 + kKeys <= Ltot;
+    const int c0 = b * BK;
+    const bool in_cache = c0 + BK <= p.Lc;
+    const bool in_new = c0 >= p.Lc && c0 + BK <= Ltot;
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
       const int q = wave + W * i;
@@ -216,11 +225,11 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
       load_share(b, buf);
       return;
     }
-    const int c0 = b * kKeys;
+    const int c0 = b * BK;
     const uint32_t kd = __builtin_amdgcn_readfirstlane(lds_offset(k_lds[buf]));
     const uint32_t vd = __builtin_amdgcn_readfirstlane(lds_offset(v_lds[buf]));
-    const bool in_cache = c0 + kKeys <= p.Lc;
-    const bool in_new = c0 >= p.Lc && c0 + kKeys <= Ltot;
+    const bool in_cache = c0 + BK <= p.Lc;
+    const bool in_new = c0 >= p.Lc && c0 + BK <= Ltot;
     if (in_cache || in_new) {
       const size_t r0 = in_cache ? (size_t)kvh * p.Lc + c0 : (size_t)kvh * p.n_new + (c0 - p.Lc);
       const uint16_t* kb = (in_cache ? p.kc : p.kn) + r0 * D;
@@ -283,46 +292,66 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
     // with block b-1, whose stage block b+kRing-1 reuses
     if constexpr (W > 1) asm volatile("s_barrier" ::: "memory");
     if (b + kRing - 1 < b1) load_block(b + kRing - 1, (b - b0 + kRing - 1) % kRing);
-    // All operand reads of a block are issued ahead of the MFMAs that use
-    // them (the scheduling barriers stop the compiler from re-serialising
-    // read, wait, MFMA): the K operands, then the QK MFMAs, then the V
-    // operands, which land while the softmax runs.
+    // The operand reads of each product are issued together ahead of its
+    // MFMAs (the scheduling barriers stop the compiler from re-serialising
+    // read, wait, MFMA): the K operands, then the QK MFMAs (one accumulator
+    // chain per 32-key block, interleaved), the V operands (see read_v), then
+    // the PV MFMAs.
     const uint32_t kl = lds_offset(k_lds[buf]);
-    bf16x8 kop[NKC];
+    bf16x8 kop[KB][NKC];
+#pragma unroll
+    for (int sb = 0; sb < KB; ++sb)
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc)
+        kop[sb][kc] = *(const lds_bf16x8*)(uintptr_t)(kl + (uint32_t)(sb * kKeys * 2 * D) +
+                                                     (k_lane ^ (32u * (uint32_t)kc)));
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 s[KB];
+#pragma unroll
+    for (int sb = 0; sb < KB; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[sb][r] = 0.f;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc)
-      kop[kc] = *(const lds_bf16x8*)(uintptr_t)(kl + (k_lane ^ (32u * (uint32_t)kc)));
-    __builtin_amdgcn_sched_barrier(0);
-    f32x16 s = {};
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qreg[kc], s, 0, 0, 0);
+      for (int sb = 0; sb < KB; ++sb)
+        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[sb][kc], qreg[kc], s[sb], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
+    // V operands, one per 16-key group of the block and 32-dim block of O^T
     const uint32_t vb = lds_offset(v_lds[buf]);
-    bf16x8 vop[2][NDB];
+    bf16x8 vop[2 * KB][NDB];
+    auto read_v = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int cst = 0; cst < 2; ++cst)
+      for (int cst = 0; cst < 2 * KB; ++cst)
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const uint32_t x = vb + (v_lane ^ (64u * (uint32_t)db));
-        i16x4 part[2];
+        for (int db = 0; db < NDB; ++db) {
+          const uint32_t x = vb + (v_lane ^ (64u * (uint32_t)db));
+          i16x4 part[2];
 #pragma unroll
-        for (int rd = 0; rd < 2; ++rd)
-          part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4*)(uintptr_t)(x + (uint32_t)((16 * cst + 8 * rd) * 2 * D)));
-        vop[cst][db] = __builtin_bit_cast(
-            bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
-      }
+          for (int rd = 0; rd < 2; ++rd)
+            part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_i16x4*)(uintptr_t)(x + (uint32_t)((16 * cst + 8 * rd) * 2 * D)));
+          vop[cst][db] = __builtin_bit_cast(
+              bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+    };
+    // one 32-key block (one wave per workgroup, registers to spare): read V
+    // now, so it lands during the softmax; two blocks: after the softmax, so
+    // that K and V operands are never live together
+    if constexpr (KB == 1) read_v();
     __builtin_amdgcn_sched_barrier(0);
-    // mask: element r of this lane is key b*32 + 8*(r/4) + 4*h + r%4 of row
-    // rho; only blocks that reach past the cache can hide keys
-    const int c0 = b * kKeys;
-    if (c0 + kKeys > p.Lc) {
+    // mask: element r of 32-key block sb of this lane is key
+    // b*BK + 32*sb + 8*(r/4) + 4*h + r%4 of row rho; only blocks that reach
+    // past the cache can hide keys
+    const int c0 = b * BK;
+    if (c0 + BK > p.Lc) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int c = c0 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (c >= vis) s[r] = -INFINITY;
-      }
+      for (int sb = 0; sb < KB; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int c = c0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (c >= vis) s[sb][r] = -INFINITY;
+        }
     }
     // Lazy running max (as in the prefill kernel): the probabilities are
     // formed against the current m_run, and only when some row-half's block
@@ -330,30 +359,38 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
     // visible block, where m_run = -inf and the sum is not finite) does the
     // wave take the block max, raise m_run, rescale O and l and redo the
     // block.  A row that sees no key yet keeps m_run = -inf and P = 0.
-    bf16x8 pb[2];
+    bf16x8 pb[2 * KB];
     float rs;
     auto exp_block = [&]() __attribute__((always_inline)) {
-      float e[16];
+      float r4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -m_run));
-      float r4[4];
+      for (int sb = 0; sb < KB; ++sb) {
+        float e[16];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) r4[j] = (e[j] + e[4 + j]) + (e[8 + j] + e[12 + j]);
+        for (int r = 0; r < 16; ++r)
+          e[r] = __builtin_amdgcn_exp2f(fmaf(s[sb][r], p.scale_log2, -m_run));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) r4[j] += (e[j] + e[4 + j]) + (e[8 + j] + e[12 + j]);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e[r];
+      }
       rs = (r4[0] + r4[1]) + (r4[2] + r4[3]);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) pb[r >> 3][r & 7] = (__bf16)e[r];
     };
     exp_block();
     if (__any(!(rs <= kSumLimit))) {
-      float mx = s[0];
+      float mx = s[0][0];
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+      for (int sb = 0; sb < KB; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[sb][r]);
       mx = fmaxf(mx, half_swap(mx));
       const float m_new = fmaxf(m_run, mx * p.scale_log2);
       if (m_new == -INFINITY) {  // nothing visible yet in this row
         rs = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) pb[r >> 3][r & 7] = (__bf16)0.f;
+        for (int g = 0; g < 2 * KB; ++g)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) pb[g][j] = (__bf16)0.f;
       } else {
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // m_run = -inf gives 0
         m_run = m_new;
@@ -366,10 +403,11 @@ __global__ void __launch_bounds__(64 * W) decode_partial_kernel(DecParams p) {
       }
     }
     l_run += rs;
-    // O^T += V^T P^T with the V operands read above
+    if constexpr (KB > 1) read_v();
+    // O^T += V^T P^T
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int cst = 0; cst < 2; ++cst)
+    for (int cst = 0; cst < 2 * KB; ++cst)
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[cst][db], pb[cst], oacc[db], 0, 0, 0);
@@ -496,12 +534,13 @@ hipError_t launch_merge_t(int n_parts, int rows, int d, const float* o_parts,
 DecodePlan plan_decode(const DecodeArgs& a) {
   DecodePlan pl;
   const int64_t keys = (int64_t)a.Lc + (a.append ? a.n_new : 0);
-  const int64_t nblk = (keys + kKeys - 1) / kKeys;
   const int64_t R = (int64_t)(a.n_q / a.n_kv) * a.n_new;
   // a GQA group of at least four 32-row blocks shares each K/V block among
   // the 8 waves of a workgroup (one workgroup per CU: its registers), else
   // one wave per workgroup (kWgPerCu per CU: their LDS)
   pl.waves = R >= 4 * kRows ? 8 : 1;
+  const int64_t bk = pl.waves == 8 ? block_keys<8>() : block_keys<1>();
+  const int64_t nblk = (keys + bk - 1) / bk;
   const int64_t n_rb = (R + kRows * pl.waves - 1) / (kRows * pl.waves);
   // one round of workgroups, at least two key blocks each
   const int64_t target = pl.waves == 1 ? 256 * kWgPerCu : 256;
