@@ -169,11 +169,12 @@ topk_gather_kernel(const float* __restrict__ scores, const uint16_t* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// Register-resident variant for Lb <= 1024 * KPT (KPT <= 32 keeps the keys in
-// registers without spills; longer local blocks use the kernel above).
-// 1024 threads; thread t
-// holds the keys of local indices KPT*t .. KPT*t + KPT-1 in registers, loaded
-// once with 16-byte vector loads.  The radix select counts into one 256-bin
+// Register-resident variant for Lb <= 1024 * KPT (up to 32 keys per thread
+// stay in registers without spills; with KPT = 64 the other 32 are staged in
+// LDS, 128 KiB, index-major so that a wave's reads are conflict-free; longer
+// local blocks use the kernel above).  1024 threads; thread t holds the keys
+// of local indices KPT*t .. KPT*t + KPT-1, loaded once with 16-byte vector
+// loads.  The radix select counts into one 256-bin
 // histogram per wave (LDS atomics collide only within a wave) and sums the
 // sixteen of them; the selected counts before each thread's range come from a
 // block scan.  Workgroup c of a head then gathers the selected rows whose
@@ -188,29 +189,40 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
                        const uint16_t* __restrict__ v, int32_t* __restrict__ out_idx,
                        uint16_t* __restrict__ out_k, uint16_t* __restrict__ out_v, int La,
                        int Lb, int lp, int head_dim, int share) {
+  constexpr int KREG = KPT < 32 ? KPT : 32;  // keys per thread in registers
+  constexpr int KLDS = KPT - KREG;           // keys per thread in LDS
   __shared__ uint32_t hist[kRegWaves][256];
   __shared__ uint32_t wsum_gt[kRegWaves], wsum_eq[kRegWaves];
   __shared__ uint32_t sel_digit, sel_above;
   __shared__ int32_t list_src[1024];
+  __shared__ uint32_t lds_key[KLDS > 0 ? KLDS * kRegThreads : 1];  // [j - KREG][thread]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y;
   const float* s = scores + (size_t)head * Lb;
   const int i0 = KPT * tid;
 
-  // ---- keys in registers; indices past Lb are marked invalid
-  uint32_t key[KPT];
+  // ---- keys in registers (and LDS); indices past Lb are marked invalid
+  uint32_t key[KREG];
+  auto put = [&](int j, uint32_t kv) __attribute__((always_inline)) {
+    if (j < KREG) key[j] = kv;
+    else lds_key[(j - KREG) * kRegThreads + tid] = kv;
+  };
   if (i0 + KPT <= Lb && ((uintptr_t)s & 15u) == 0) {
 #pragma unroll
     for (int j = 0; j < KPT; j += 4) {
       const float4 f = *reinterpret_cast<const float4*>(s + i0 + j);
-      key[j] = score_key(f.x); key[j + 1] = score_key(f.y);
-      key[j + 2] = score_key(f.z); key[j + 3] = score_key(f.w);
+      put(j, score_key(f.x)); put(j + 1, score_key(f.y));
+      put(j + 2, score_key(f.z)); put(j + 3, score_key(f.w));
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) key[j] = i0 + j < Lb ? score_key(s[i0 + j]) : 0u;
+    for (int j = 0; j < KPT; ++j) put(j, i0 + j < Lb ? score_key(s[i0 + j]) : 0u);
   }
+  // key j of this thread (each thread reads back only its own LDS slots)
+  auto get = [&](int j) __attribute__((always_inline)) -> uint32_t {
+    return j < KREG ? key[j] : lds_key[(j - KREG) * kRegThreads + tid];
+  };
   const int n_valid = max(0, min(KPT, Lb - i0));
 
   // every share slot is filled below (exactly lp distinct positions are
@@ -224,9 +236,11 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
     for (int b = lane; b < 256; b += 64) hist[wave][b] = 0u;
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < KPT; ++j)
-      if (j < n_valid && (key[j] & prefix_mask) == prefix)
-        atomicAdd(&hist[wave][(key[j] >> shift) & 255u], 1u);
+    for (int j = 0; j < KPT; ++j) {
+      const uint32_t kj = get(j);
+      if (j < n_valid && (kj & prefix_mask) == prefix)
+        atomicAdd(&hist[wave][(kj >> shift) & 255u], 1u);
+    }
     __syncthreads();
     if (tid < 64) {
       // lane L owns bins 4L..4L+3 (summed over the waves' histograms)
@@ -268,8 +282,9 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
   uint32_t n_gt = 0u, n_eq = 0u;
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
-    n_gt += (j < n_valid && key[j] > T) ? 1u : 0u;
-    n_eq += (j < n_valid && key[j] == T) ? 1u : 0u;
+    const uint32_t kj = get(j);
+    n_gt += (j < n_valid && kj > T) ? 1u : 0u;
+    n_eq += (j < n_valid && kj == T) ? 1u : 0u;
   }
   uint32_t x_gt = n_gt, x_eq = n_eq;  // inclusive wave scans
   for (int off = 1; off < 64; off <<= 1) {
@@ -285,8 +300,9 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
   const int p0 = blockIdx.x * share, p1 = min(lp, p0 + share);
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
-    const bool gt = j < n_valid && key[j] > T;
-    const bool eq = j < n_valid && key[j] == T;
+    const uint32_t kj = get(j);
+    const bool gt = j < n_valid && kj > T;
+    const bool eq = j < n_valid && kj == T;
     const uint32_t pos = gt_before + min(eq_before, need);
     const bool sel = gt || (eq && eq_before < need);
     if (sel && (int)pos >= p0 && (int)pos < p1) {
@@ -323,7 +339,7 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
 
 hipError_t launch_compress(const CompressArgs& a, hipStream_t stream) {
   if (a.lp == 0) return hipSuccess;
-  if (a.Lb <= kRegThreads * 32) {
+  if (a.Lb <= kRegThreads * 64) {
     // a share of at most 1024 output rows per workgroup, about 64 rows each
     // for the gather, at most 32 workgroups per head
     int groups = (a.lp + 63) / 64;
@@ -340,8 +356,11 @@ hipError_t launch_compress(const CompressArgs& a, hipStream_t stream) {
     else if (a.Lb <= kRegThreads * 16)
       hipLaunchKernelGGL(topk_gather_reg_kernel<16>, grid, dim3(kRegThreads), 0, stream, a.scores,
                          a.k, a.v, a.idx, a.out_k, a.out_v, a.La, a.Lb, a.lp, a.head_dim, share);
-    else
+    else if (a.Lb <= kRegThreads * 32)
       hipLaunchKernelGGL(topk_gather_reg_kernel<32>, grid, dim3(kRegThreads), 0, stream, a.scores,
+                         a.k, a.v, a.idx, a.out_k, a.out_v, a.La, a.Lb, a.lp, a.head_dim, share);
+    else
+      hipLaunchKernelGGL(topk_gather_reg_kernel<64>, grid, dim3(kRegThreads), 0, stream, a.scores,
                          a.k, a.v, a.idx, a.out_k, a.out_v, a.La, a.Lb, a.lp, a.head_dim, share);
     return hipGetLastError();
   }
