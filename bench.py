@@ -280,7 +280,10 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float =
             "decode_gbs": round(dec_bytes / (dec_us * 1e-6) / 1e9, 1),
             "decode_hbm_frac": round(dec_bytes / (dec_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
             "merge_us": round(mrg_us, 2), "merge_algorithmic_bytes": mrg_bytes,
-            "kernel": "decode_partial_kernel<128> + merge_kernel",
+            # the library's plan: eight-wave ping-pong workgroups once a GQA
+            # group has four 32-row blocks, one-wave workgroups below that
+            "kernel": ("decode_pingpong_kernel" if (n_q // n_kv) * n_new >= 128 else "decode_partial_kernel")
+            + f"<{d}> + merge_kernel",
             "bound": "hbm", "timing": f"median of {steps} back-to-back launches, HIP events",
             "cpu_baseline": cpu}
 
