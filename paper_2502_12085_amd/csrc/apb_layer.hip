@@ -13,7 +13,10 @@
 // the N side, a 256 x 256 workgroup tile of 4 waves (2 x 2, each 128
 // features x 128 tokens, one wave per SIMD, accumulators in AGPRs), K steps
 // of 64 whose weight and token slabs are copied HBM -> LDS by
-// global_load_lds_dwordx4 into XOR-swizzled tiles in two stages.  The step
+// global_load_lds_dwordx4 into XOR-swizzled tiles in two stages.  Neither a
+// copy nor an operand read spends a vector instruction on its address: a
+// copy is a scalar base plus a fixed per-lane offset, a read one XOR of a
+// per-lane base plus an instruction offset.  The step
 // boundary is software-pipelined: at its last 16-deep substep a wave waits
 // for its copies of the next step, passes the barrier, and issues that
 // substep's MFMAs with the next step's first operand reads and the copies of
@@ -93,62 +96,63 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
   // ---- copies: piece j (8 rows x 128 bytes) of each slab; wave w copies
   // pieces 8w .. 8w+7.  Lane l takes row l/8 of the piece and fetches the
   // chunk that belongs at slot l%8.  Rows past the last feature or token
-  // repeat it (their results are never stored).
+  // repeat it (their results are never stored).  A copy is a scalar base (the
+  // operand's first row for this workgroup, advanced by the K step in scalar
+  // registers) plus a fixed per-lane byte offset: no vector instruction.
   const int cp_row = lane >> 3, cp_slot = lane & 7;
-  const uint16_t* w_src[kPieces];
-  const uint16_t* x_src[kPieces];
+  const int x_ld = XM == kXHeadMajor ? p.dh : p.K;  // elements between token rows
+  uint32_t w_off[kPieces], x_off[kPieces];
 #pragma unroll
   for (int i = 0; i < kPieces; ++i) {
     const int rho = 8 * (kPieces * wave + i) + cp_row;  // slab row 0..255
     const int chunk = 8 * (cp_slot ^ swz(rho));
-    int fr;
-    const uint16_t* wm_base = p.w;
-    if constexpr (WM == kWGateUp) {
-      const int half = rho >> 7, q = rho & 127;
-      fr = f0 + 64 * half + (q & 63);
-      if (q >= 64) wm_base = p.w_up;
-    } else {
-      fr = f0 + rho;
-    }
+    int fr = WM == kWGateUp ? f0 + 64 * (rho >> 7) + (rho & 63) : f0 + rho;
     fr = min(fr, p.F - 1);
-    w_src[i] = wm_base + (size_t)fr * p.K + chunk;
+    w_off[i] = 2u * (uint32_t)((fr - f0) * p.K + chunk);
     const int tr = min(t0 + rho, p.T - 1);
-    if constexpr (XM == kXHeadMajor)
-      x_src[i] = p.x + (size_t)tr * p.dh + chunk;
-    else
-      x_src[i] = p.x + (size_t)tr * p.K + chunk;
+    x_off[i] = 2u * (uint32_t)((tr - t0) * x_ld + chunk);
   }
+  const uint16_t* const w_first = p.w + (size_t)f0 * p.K;
+  const uint16_t* const w_up_first = (WM == kWGateUp ? p.w_up : p.w) + (size_t)f0 * p.K;
+  const uint16_t* const x_first = p.x + (size_t)t0 * x_ld;
   // copy q (0..15) of step kk into stage st: q < 8 weight pieces, else token pieces
   auto copy = [&](int kk, int st, int q) __attribute__((always_inline)) {
     const int k0 = kk * kBK;
     const int i = q & 7;
     const int j = kPieces * wave + i;
     if (q < 8) {
+      // gate/up: rows 64..127 of either 128-row half are up-projection rows
+      const uint16_t* base =
+          (WM == kWGateUp && ((kPieces * wave + i) & 15) >= 8 ? w_up_first : w_first) + k0;
       const uint32_t d = __builtin_amdgcn_readfirstlane(lds_offset(&a_lds[st][j * 512]));
-      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(w_src[i] + k0),
+      asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(w_off[i]), "s"(base),
                    "s"(d)
-                   : "memory", "m0");
+                   : "memory");
     } else {
-      size_t xoff = (size_t)k0;
-      if constexpr (XM == kXHeadMajor) xoff = (size_t)(k0 / p.dh) * p.T * p.dh + (k0 % p.dh);
+      // head-major tokens: K element k0 is column k0 % dh of head k0 / dh
+      const size_t xoff = XM == kXHeadMajor ? (size_t)(k0 / p.dh) * p.T * p.dh + (k0 % p.dh) : (size_t)k0;
+      const uint16_t* base = x_first + xoff;
       const uint32_t d = __builtin_amdgcn_readfirstlane(lds_offset(&b_lds[st][j * 512]));
-      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(x_src[i] + xoff),
+      asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(x_off[i]), "s"(base),
                    "s"(d)
-                   : "memory", "m0");
+                   : "memory");
     }
   };
 
   // ---- operands: lane (n, h) of an MFMA block reads slab row 32*blk + n,
-  // K elements 16*kc + 8*h .. +7, i.e. chunk 2*kc + h of that row
-  auto a_read = [&](int st, int mb, int kc) __attribute__((always_inline)) -> bf16x8 {
-    const int row = 128 * wm + 32 * mb + n;
-    return *(const lds_bf16x8*)(uintptr_t)(lds_offset(a_lds[st]) + row * 128 +
-                                            16 * ((2 * kc + h) ^ swz(row)));
-  };
-  auto b_read = [&](int st, int nb, int kc) __attribute__((always_inline)) -> bf16x8 {
-    const int row = 128 * wn + 32 * nb + n;
-    return *(const lds_bf16x8*)(uintptr_t)(lds_offset(b_lds[st]) + row * 128 +
-                                            16 * ((2 * kc + h) ^ swz(row)));
+  // K elements 16*kc + 8*h .. +7, i.e. chunk 2*kc + h of that row, stored at
+  // slot (2*kc + h) ^ swz(row).  swz(row) = (n >> 1) & 7 for every block, so
+  // the address is (lane base ^ 32*kc) plus a constant for stage and block.
+  const int sw = (n >> 1) & 7;
+  const uint32_t lane_chunk = (uint32_t)(32 * (sw >> 1) + 16 * (h ^ (sw & 1)));
+  const uint32_t a_lane = (uint32_t)((128 * wm + n) * 128) + lane_chunk;
+  const uint32_t b_lane = (uint32_t)((128 * wn + n) * 128) + lane_chunk;
+  // stage st's row bases (the stages are 32 KiB apart, so the XOR with 32*kc
+  // below touches only the chunk bits)
+  auto a_base = [&](int st) __attribute__((always_inline)) { return lds_offset(a_lds[st]) + a_lane; };
+  auto b_base = [&](int st) __attribute__((always_inline)) { return lds_offset(b_lds[st]) + b_lane; };
+  auto read = [](uint32_t base, int blk, int kc) __attribute__((always_inline)) -> bf16x8 {
+    return *(const lds_bf16x8*)(uintptr_t)((base ^ (32u * (uint32_t)kc)) + 4096u * (uint32_t)blk);
   };
 
   f32x16 acc[4][4];
@@ -170,9 +174,9 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
     for (int q = 0; q < 16; ++q) copy(1, 1, q);
   }
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) av[0][mb] = a_read(0, mb, 0);
+  for (int mb = 0; mb < 4; ++mb) av[0][mb] = read(a_base(0), mb, 0);
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) bv[0][nb] = b_read(0, nb, 0);
+  for (int nb = 0; nb < 4; ++nb) bv[0][nb] = read(b_base(0), nb, 0);
 
   // One K step in four substeps of 16 MFMAs, each followed by the next
   // substep's eight operand reads.  NEXT: step kk+1 exists (at the last
@@ -181,6 +185,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
   auto step = [&](int kk, auto next_t, auto copy_t) __attribute__((always_inline)) {
     constexpr bool NEXT = decltype(next_t)::value, COPY = decltype(copy_t)::value;
     const int st = kk & 1;
+    const uint32_t ab = a_base(st), bb = b_base(st), ab1 = a_base(st ^ 1), bb1 = b_base(st ^ 1);
 #pragma unroll
     for (int kc = 0; kc < 4; ++kc) {
       const int cur = kc & 1, nxt = cur ^ 1;
@@ -196,11 +201,11 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[cur][mb], bv[cur][nb],
                                                               acc[mb][nb], 0, 0, 0);
         if (!boundary) {
-          if (i < 4) av[nxt][i] = a_read(st, i, kc + 1);
-          else if (i < 8) bv[nxt][i - 4] = b_read(st, i - 4, kc + 1);
+          if (i < 4) av[nxt][i] = read(ab, i, kc + 1);
+          else if (i < 8) bv[nxt][i - 4] = read(bb, i - 4, kc + 1);
         } else if (NEXT) {
-          if (i < 4) av[nxt][i] = a_read(st ^ 1, i, 0);
-          else if (i < 8) bv[nxt][i - 4] = b_read(st ^ 1, i - 4, 0);
+          if (i < 4) av[nxt][i] = read(ab1, i, 0);
+          else if (i < 8) bv[nxt][i - 4] = read(bb1, i - 4, 0);
           if (COPY) copy(kk + 2, st, i);
         }
         __builtin_amdgcn_sched_barrier(0);
