@@ -269,7 +269,7 @@ attn_fwd_kernel(Params p) {
             "global_load_lds_dwordx4 %3, %4 offset:3072" ::"v"(cp_off[4 * g]),
             "v"(cp_off[4 * g + 1]), "v"(cp_off[4 * g + 2]), "v"(cp_off[4 * g + 3]), "s"(base),
             "s"(dst)
-            : "memory", "m0");
+            : "memory");
       }
     } else {
       // tile straddles a segment end (or the end of the keys): rows are
@@ -283,7 +283,7 @@ attn_fwd_kernel(Params p) {
         const int swz = copies_v ? v_swz<D>(row) : k_swz<D>(row);
         const uint16_t* src = key_row_sel<D>(p, cp_loc, cp_pass, kvh, c) + 8 * (slot ^ swz);
         asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst)
-                     : "memory", "m0");
+                     : "memory");
       }
     }
   };
@@ -342,11 +342,11 @@ attn_fwd_kernel(Params p) {
     v_lane = (uint32_t)(row * 2 * D + 64 * (row & (NDB - 1)) + 16 * (2 * (g & 1) + ((sl & 3) >> 1)) +
                         8 * (sl & 1));
   }
-  auto k_operand = [&](uint32_t kb, int i) -> bf16x8 __attribute__((always_inline)) {
+  auto k_operand = [&](uint32_t kb, int i) __attribute__((always_inline)) -> bf16x8 {
     const uint32_t a = (kb ^ (32u * (uint32_t)(i / kKB))) + (uint32_t)(64 * D * (i % kKB));
     return *(const lds_bf16x8*)(uintptr_t)a;
   };
-  auto v_operand = [&](uint32_t vb, int i) -> bf16x8 __attribute__((always_inline)) {
+  auto v_operand = [&](uint32_t vb, int i) __attribute__((always_inline)) -> bf16x8 {
     const int c = i / NDB, db = i % NDB;
     const uint32_t x = vb ^ (64u * (uint32_t)db);
     i16x4 part[2];

@@ -479,11 +479,11 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
     v_lane = (uint32_t)(row * 2 * D + 64 * (row & (NDB - 1)) +
                         16 * (2 * (g & 1) + ((sl & 3) >> 1)) + 8 * (sl & 1));
   }
-  auto k_operand = [&](uint32_t kb, int i) -> bf16x8 __attribute__((always_inline)) {
+  auto k_operand = [&](uint32_t kb, int i) __attribute__((always_inline)) -> bf16x8 {
     const uint32_t a = (kb ^ (32u * (uint32_t)(i / KB))) + (uint32_t)(kKeys * 2 * D * (i % KB));
     return *(const lds_bf16x8*)(uintptr_t)a;
   };
-  auto v_operand = [&](uint32_t vb, int i) -> bf16x8 __attribute__((always_inline)) {
+  auto v_operand = [&](uint32_t vb, int i) __attribute__((always_inline)) -> bf16x8 {
     const int c = i / NDB, db = i % NDB;
     const uint32_t x = vb ^ (64u * (uint32_t)db);
     i16x4 part[2];
