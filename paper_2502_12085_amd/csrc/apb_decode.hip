@@ -13,13 +13,15 @@
 // partial (O / l, lse) in fp32 to a caller-provided workspace; the merge
 // kernel then combines the splits into the host's partial.  Few rows per KV
 // head (one generated token): one-wave workgroups of one 32-row block each.
-// Many rows (the question tokens): eight-wave workgroups that share each K/V
-// block among 256 rows and alternate MFMA and softmax phases between two
-// wave groups.
+// Many rows (the question tokens): eight-wave workgroups that share each
+// 128-key K/V tile among 256 rows and alternate MFMA and softmax phases
+// between two wave groups, on the prefill kernel's schedule.
 //  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (32 keys on M, 32 rows on N).
-//  * K and V blocks are copied HBM -> LDS with global_load_lds_dwordx4 into
-//    XOR-swizzled row-major tiles, a three-stage ring, so the copies of
-//    later blocks fly while block b is computed.  K is read back with
+//  * K and V are copied HBM -> LDS with global_load_lds_dwordx4 into
+//    XOR-swizzled row-major tiles while earlier ones are computed (32-key
+//    blocks through a three-stage ring for one wave; 128-key tiles through
+//    two-stage rings, K and V copied in different phases, for eight).  K is
+//    read back with
 //    ds_read_b128 as the A operand of S^T; V is read back transposed with
 //    ds_read_b64_tr_b16 as the A operand of O^T = V^T P^T, and P comes
 //    straight from the S^T accumulator layout.
@@ -112,10 +114,10 @@ __device__ __forceinline__ const uint16_t* kv_row(const DecParams& p, const uint
                   : fresh + ((size_t)kvh * p.n_new + (c - p.Lc)) * D;
 }
 
-// Keys per ring block of the eight-wave kernel: two 32-key MFMA blocks, so
-// that a block's wait and barriers are paid once per 64 keys and its QK
-// products run as two independent accumulator chains.
-constexpr int kPingPongKB = 2;
+// Keys per tile of the eight-wave kernel: four 32-key MFMA blocks, so that a
+// phase holds 64 MFMAs (the most the registers allow, as in the prefill
+// kernel) and its QK products run as four independent accumulator chains.
+constexpr int kPingPongKB = 4;
 
 // Few rows per KV head (one generated token): a one-wave workgroup owns the
 // 32-row block blockIdx.z (kWgPerCu of them share a CU's LDS) and streams
@@ -369,38 +371,41 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
 }
 
 // Many rows per KV head (the question tokens): eight waves, each owning a
-// 32-row block, share every 64-key K/V block of a three-stage LDS ring, and
-// work as two groups of four (one wave of each per SIMD) that alternate
-// between an MFMA phase {S(b) = K(b) Q^T, O += P(b-1) V(b-1)} and a softmax
-// phase one phase apart, as in the prefill kernel: on every SIMD one wave
-// feeds the matrix core while the other runs its softmax.  Group A runs the
-// MFMA step of block k in phase 2k and its softmax in phase 2k+1, group B one
-// phase later; every wave copies its share of block k+1 at the start of
-// phase 2k and waits for it at the end of phase 2k+1 (a barrier ends every
-// phase).  Block k+1 goes into the stage of block k-2, whose last reader (the
-// PV product of group B) ran in phase 2k-1.
+// 32-row block, share every 128-key K/V tile of the split, on the prefill
+// kernel's schedule.  The waves form two groups of four (one wave of each per
+// SIMD) that alternate between an MFMA phase {S(t) = K(t) Q^T, O += P(t-1)
+// V(t-1)} and a softmax phase one phase apart: on every SIMD one wave feeds
+// the matrix core while the other runs its softmax, and a phase is 64 MFMAs
+// long, so its fixed cost (barrier, first operand reads, drain) is spread
+// over as much work as the registers allow.  K and V tiles go through
+// two-stage rings (128 KiB): group B copies K(T) at the start of phase 2T-2
+// (its softmax phase; K(T-2) was last read in phase 2T-3) and waits for it at
+// the end of phase 2T-1; group A copies V(T) behind the first operand reads
+// of phase 2T (its MFMA phase; V(T-2) was last read in phase 2T-1) and waits
+// for it at the end of phase 2T+1.  Tile indices are relative to the split.
 template <int D>
 __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
   constexpr int W = 8;
-  constexpr int KB = kPingPongKB;            // 32-key MFMA blocks per ring block
-  constexpr int BK = KB * kKeys;             // keys per ring block
+  constexpr int GW = W / 2;                  // waves per group
+  constexpr int KB = kPingPongKB;            // 32-key MFMA blocks per tile
+  constexpr int BK = KB * kKeys;             // keys per tile
   constexpr int NKC = D / 16;                // MFMA k-steps over head_dim
   constexpr int NDB = D / 32;                // 32-dim blocks of O^T
   constexpr int KCH = D / 8;                 // 16-byte chunks per row
   constexpr int PIECES = BK * D / 512;       // 1 KiB copies per K or V tile
   constexpr int ROWS_PER_PIECE = 512 / D;
-  constexpr int CPW = 2 * PIECES / W;        // copies per wave per block
-  constexpr int NQK = KB * NKC;              // QK MFMAs per block
+  constexpr int WP = PIECES / GW;            // copies per wave per tile (one tensor)
+  constexpr int NQK = KB * NKC;              // QK MFMAs per tile
   constexpr int NPG = BK / 16;               // 16-key groups of P (PV k-steps)
-  constexpr int NPV = NPG * NDB;             // PV MFMAs per block
+  constexpr int NPV = NPG * NDB;             // PV MFMAs per tile
   constexpr int PD = 2;                      // operand read-ahead (MFMA steps)
-  static_assert(CPW * W == 2 * PIECES && NQK == NPV, "tile split");
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kRing][BK * D];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kRing][BK * D];
+  static_assert(WP * GW == PIECES && WP % 4 == 0 && NQK == NPV, "tile split");
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][BK * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][BK * D];
 
   const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int grp = wave / 4;
+  const int grp = wave / GW, wig = wave % GW;
   const int split = blockIdx.x, kvh = blockIdx.y, rb = blockIdx.z * W + wave;
   const int Ltot = p.Lc + (p.append ? p.n_new : 0);
   const int nblk = (Ltot + BK - 1) / BK;
@@ -425,45 +430,61 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
     }
   }
 
-  // copies: this wave's share, piece q = wave + W*i of the 2*PIECES pieces
-  // (K pieces first, then V); a block inside one segment (cache or new
-  // rows) takes one scalar base and one M0 per piece, a block straddling the
-  // cache end or the last key looks its rows up one by one
-  auto load_share = [&](int b, int buf) __attribute__((always_inline)) {
-    const int c0 = b * BK;
+  // Copies of tile T (keys (b0 + T) * BK ..): group A copies V, group B K;
+  // wave wig of a group copies pieces wig*WP .. +WP-1 of the tile.  Inside one
+  // segment (cache or new rows) one M0 serves four pieces: the instruction
+  // offset moves the LDS destination and the source by the same 1 KiB, the
+  // per-lane offsets carry the rest.  A tile that straddles the cache end or
+  // the last key looks its rows up one by one (rows past the last key repeat
+  // it and are masked).
+  const bool copies_v = grp == 0;
+  const uint16_t* cp_cache = copies_v ? p.vc : p.kc;
+  const uint16_t* cp_new = copies_v ? p.vn : p.kn;
+  uint32_t cp_off[WP];  // per-lane byte offset of piece j, less (j % 4) KiB
+#pragma unroll
+  for (int j = 0; j < WP; ++j) {
+    const int row = (wig * WP + j) * ROWS_PER_PIECE + lane / KCH;
+    const int slot = lane % KCH;
+    const int swz = copies_v ? v_swz<D>(row) : k_swz<D>(row);
+    cp_off[j] = 2u * (uint32_t)(row * D + 8 * (slot ^ swz)) - 1024u * (j % 4);
+  }
+  auto issue = [&](int T) __attribute__((always_inline)) {
+    const int c0 = (b0 + T) * BK;
+    uint16_t* stage = copies_v ? v_lds[T % 2] : k_lds[T % 2];
     const bool in_cache = c0 + BK <= p.Lc;
     const bool in_new = c0 >= p.Lc && c0 + BK <= Ltot;
-    // the lane's copy slot is recomputed here (the opaque copy of the lane
-    // index keeps the compiler from holding four offsets live across the
-    // block loop, where they would be spilled)
-    int lane_c = lane;
-    asm volatile("" : "+v"(lane_c));
-    const int cp_row0 = lane_c / KCH, cp_slot = lane_c % KCH;
+    if (in_cache || in_new) {
+      const uint16_t* base = in_cache ? cp_cache + ((size_t)kvh * p.Lc + c0) * D
+                                      : cp_new + ((size_t)kvh * p.n_new + (c0 - p.Lc)) * D;
 #pragma unroll
-    for (int i = 0; i < CPW; ++i) {
-      const int q = wave + W * i;
-      const bool is_v = q >= PIECES;
-      const int j = is_v ? q - PIECES : q;
-      const int row = j * ROWS_PER_PIECE + cp_row0;
-      const int swz = is_v ? v_swz<D>(row) : k_swz<D>(row);
-      const uint32_t dst = __builtin_amdgcn_readfirstlane(
-          lds_offset(is_v ? &v_lds[buf][j * 512] : &k_lds[buf][j * 512]));
-      if (in_cache || in_new) {
-        const size_t r0 = in_cache ? (size_t)kvh * p.Lc + c0 : (size_t)kvh * p.n_new + (c0 - p.Lc);
-        const uint16_t* base = (is_v ? (in_cache ? p.vc : p.vn) : (in_cache ? p.kc : p.kn)) + r0 * D;
-        const uint32_t off = 2u * (uint32_t)(row * D + 8 * (cp_slot ^ swz));
-        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
-                     "s"(dst)
-                     : "memory");
-      } else {
+      for (int g = 0; g < WP / 4; ++g) {
+        const uint32_t dst =
+            __builtin_amdgcn_readfirstlane(lds_offset(&stage[(wig * WP + 4 * g) * 512]));
+        asm volatile(
+            "s_mov_b32 m0, %5\n\t"
+            "global_load_lds_dwordx4 %0, %4\n\t"
+            "global_load_lds_dwordx4 %1, %4 offset:1024\n\t"
+            "global_load_lds_dwordx4 %2, %4 offset:2048\n\t"
+            "global_load_lds_dwordx4 %3, %4 offset:3072" ::"v"(cp_off[4 * g]),
+            "v"(cp_off[4 * g + 1]), "v"(cp_off[4 * g + 2]), "v"(cp_off[4 * g + 3]), "s"(base),
+            "s"(dst)
+            : "memory");
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < WP; ++j) {
+        const uint32_t dst = lds_offset(&stage[(wig * WP + j) * 512]);
+        const int row = (wig * WP + j) * ROWS_PER_PIECE + lane / KCH;
+        const int slot = lane % KCH;
         const int c = min(c0 + row, Ltot - 1);
-        const uint16_t* src = kv_row<D>(p, is_v ? p.vc : p.kc, is_v ? p.vn : p.kn, kvh, c) +
-                              8 * (cp_slot ^ swz);
+        const int swz = copies_v ? v_swz<D>(row) : k_swz<D>(row);
+        const uint16_t* src = kv_row<D>(p, cp_cache, cp_new, kvh, c) + 8 * (slot ^ swz);
         asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst)
                      : "memory");
       }
     }
   };
+  // every wave has at most one tile's copies in flight when it waits
   auto land = []() __attribute__((always_inline)) { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
   auto barrier = []() __attribute__((always_inline)) {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -512,17 +533,19 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
   auto pv_step = [&](const bf16x8& a, int i) __attribute__((always_inline)) {
     oacc[i % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[i / NDB], oacc[i % NDB], 0, 0, 0);
   };
-  auto k_stage = [&](int k) __attribute__((always_inline)) { return lds_offset(k_lds[k % kRing]) + k_lane; };
-  auto v_stage = [&](int k) __attribute__((always_inline)) { return lds_offset(v_lds[k % kRing]) + v_lane; };
-  // S of block k (ring index) with O += P V of block k-1, interleaved
-  auto qk_pv = [&](int k) __attribute__((always_inline)) {
-    const uint32_t kl = k_stage(k), vl = v_stage(k - 1);
+  auto k_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(k_lds[t % 2]) + k_lane; };
+  auto v_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(v_lds[t % 2]) + v_lane; };
+  // S of tile t with O += P V of tile t-1, interleaved; copy_v: group A's
+  // V(t) copies, issued behind the phase's first operand reads
+  auto qk_pv = [&](int t, bool copy_v) __attribute__((always_inline)) {
+    const uint32_t kl = k_stage(t), vl = v_stage(t - 1);
     bf16x8 ka[PD + 1], va[PD + 1];
 #pragma unroll
     for (int i = 0; i < PD; ++i) {
       ka[i] = k_operand(kl, i);
       va[i] = v_operand(vl, i);
     }
+    if (copy_v) issue(t);
 #pragma unroll
     for (int i = 0; i < NQK; ++i) {
       if (i + PD < NQK) {
@@ -534,11 +557,12 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto qk_only = [&](int k) __attribute__((always_inline)) {
-    const uint32_t kl = k_stage(k);
+  auto qk_only = [&](int t, bool copy_v) __attribute__((always_inline)) {
+    const uint32_t kl = k_stage(t);
     bf16x8 ka[PD + 1];
 #pragma unroll
     for (int i = 0; i < PD; ++i) ka[i] = k_operand(kl, i);
+    if (copy_v) issue(t);
 #pragma unroll
     for (int i = 0; i < NQK; ++i) {
       if (i + PD < NQK) ka[(i + PD) % (PD + 1)] = k_operand(kl, i + PD);
@@ -546,8 +570,8 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto pv_only = [&](int k) __attribute__((always_inline)) {
-    const uint32_t vl = v_stage(k);
+  auto pv_only = [&](int t) __attribute__((always_inline)) {
+    const uint32_t vl = v_stage(t);
     bf16x8 va[PD + 1];
 #pragma unroll
     for (int i = 0; i < PD; ++i) va[i] = v_operand(vl, i);
@@ -558,46 +582,54 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // softmax of block b0+k: mask, lazy running max, exp2, row sums, P -> bf16
-  auto softmax = [&](int k) __attribute__((always_inline)) {
-    const int c0 = (b0 + k) * BK;
-    if (c0 + BK > p.Lc) {  // only blocks that reach past the cache can hide keys
+  // Softmax of tile t: mask, lazy running max, exp2, row sums, P -> bf16,
+  // one 32-key block at a time in three batches (its FMAs, its exp2, its sums
+  // and packing).  A row that sees no key of the split yet keeps m_run = -inf
+  // and P = 0.
+  auto softmax = [&](int t) __attribute__((always_inline)) {
+    const int c0 = (b0 + t) * BK;
+    if (c0 + BK > p.Lc) {  // only tiles that reach past the cache can hide keys
 #pragma unroll
-      for (int sb = 0; sb < KB; ++sb)
+      for (int b = 0; b < KB; ++b)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int c = c0 + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (c >= vis) s[sb][r] = -INFINITY;
+          const int c = c0 + 32 * b + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (c >= vis) s[b][r] = -INFINITY;
         }
     }
-    float rs;
-    auto exp_block = [&]() __attribute__((always_inline)) {
-      float r4[4] = {0.f, 0.f, 0.f, 0.f};
+    float rs[4];
+    auto exp_tile = [&]() __attribute__((always_inline)) {
 #pragma unroll
-      for (int sb = 0; sb < KB; ++sb) {
-        float e[16];
+      for (int j = 0; j < 4; ++j) rs[j] = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) e[r] = fmaf(s[sb][r], p.scale_log2, -m_run);
+      for (int b = 0; b < KB; ++b) {
+        f32x16 e;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) e[r] = fmaf(s[b][r], p.scale_log2, -m_run);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(e[r]);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) r4[j] += (e[j] + e[4 + j]) + (e[8 + j] + e[12 + j]);
+        for (int k = 0; k < 4; ++k)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) pb[2 * sb + (r >> 3)][r & 7] = (__bf16)e[r];
+          for (int j = 0; j < 4; ++j) rs[j] += e[4 * j + k];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pb[2 * b + (r >> 3)][r & 7] = (__bf16)e[r];
       }
-      rs = (r4[0] + r4[1]) + (r4[2] + r4[3]);
     };
-    exp_block();
-    if (__any(!(rs <= kSumLimit))) {
+    exp_tile();
+    if (__any(!((rs[0] + rs[1]) + (rs[2] + rs[3]) <= kSumLimit))) {
       float mx = s[0][0];
 #pragma unroll
-      for (int sb = 0; sb < KB; ++sb)
+      for (int b = 0; b < KB; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[sb][r]);
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[b][r]);
       mx = fmaxf(mx, half_swap(mx));
       const float m_new = fmaxf(m_run, mx * p.scale_log2);
       if (m_new == -INFINITY) {  // nothing visible yet in this row
-        rs = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) rs[j] = 0.f;
 #pragma unroll
         for (int g = 0; g < NPG; ++g)
 #pragma unroll
@@ -610,35 +642,34 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
         for (int db = 0; db < NDB; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-        exp_block();
+        exp_tile();
       }
     }
-    l_run += rs;
+    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
   };
   auto mfma_prio = []() __attribute__((always_inline)) { __builtin_amdgcn_s_setprio(1); };
   auto base_prio = []() __attribute__((always_inline)) { __builtin_amdgcn_s_setprio(0); };
 
-  // Both groups pass 2*nb + 3 barriers (a split always owns at least one
-  // block unless there are no keys at all, when nobody enters).
+  // Both groups pass 2*nb + 3 barriers (a split owns at least one tile
+  // unless there are no keys at all, when nobody enters).
   if (nb > 0) {
-    load_share(b0, 0);
-    land();
-    // Q is taken into registers here, where its loads have landed with block
-    // 0 (left to itself, the compiler waits for them at their first use,
-    // after later copies have been issued, and so also for those copies)
-#pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) asm volatile("" : "+v"(qreg[kc]));
-    barrier();
     if (grp == 0) {
-      for (int k = 0; k < nb; ++k) {
-        if (k + 1 < nb) load_share(b0 + k + 1, (k + 1) % kRing);
+      // group A: copies V; MFMA(t) in phase 2t, softmax(t) in phase 2t+1
+      barrier();  // K(0) landed (copied by group B)
+      mfma_prio();
+      qk_only(0, true);
+      base_prio();
+      barrier();
+      softmax(0);
+      land();  // V(0)
+      barrier();
+      for (int t = 1; t < nb; ++t) {
         mfma_prio();
-        if (k == 0) qk_only(0);
-        else qk_pv(k);
+        qk_pv(t, true);
         base_prio();
         barrier();
-        softmax(k);
-        if (k + 1 < nb) land();
+        softmax(t);
+        land();  // V(t)
         barrier();
       }
       mfma_prio();
@@ -647,19 +678,29 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
       barrier();
       barrier();
     } else {
-      if (1 < nb) load_share(b0 + 1, 1);
+      // group B: copies K; MFMA(t) in phase 2t+1, softmax(t) in phase 2t+2
+      issue(0);
+      land();  // K(0)
       barrier();
-      for (int k = 0; k < nb; ++k) {
-        mfma_prio();
-        if (k == 0) qk_only(0);
-        else qk_pv(k);
-        base_prio();
-        if (k + 1 < nb) land();
+      if (1 < nb) issue(1);
+      barrier();
+      mfma_prio();
+      qk_only(0, false);
+      base_prio();
+      land();  // K(1)
+      barrier();
+      for (int t = 1; t < nb; ++t) {
+        if (t + 1 < nb) issue(t + 1);
+        softmax(t - 1);
         barrier();
-        if (k + 2 < nb) load_share(b0 + k + 2, (k + 2) % kRing);
-        softmax(k);
+        mfma_prio();
+        qk_pv(t, false);
+        base_prio();
+        land();  // K(t+1)
         barrier();
       }
+      softmax(nb - 1);
+      barrier();
       mfma_prio();
       pv_only(nb - 1);
       base_prio();
