@@ -52,6 +52,14 @@ def _run_decode(q, kc, vc, kn, vn, n_q, n_kv, d, scale=0.0):
     (4, 4, 128, 513, 130, 1),     # no GQA, 130 causal new tokens over a ragged cache
     (8, 2, 128, 0, 64, 1),        # empty cache, 256 rows of new tokens alone
     (56, 8, 128, 100, 20, 0),     # few keys (four blocks), 140 rows, no append
+    # eight-wave path, 128-key tiles: cache ends on, just past and just before
+    # a tile edge, one-tile splits, one cached key, row groups past 256
+    (15, 3, 128, 129, 50, 0),     # 250 rows, cache one key past a tile edge, no append
+    (10, 2, 64, 1, 67, 1),        # one cached key, then 67 causal new tokens
+    (1, 1, 64, 1000, 391, 1),     # no GQA, 391 rows (two row groups), long new block
+    (6, 3, 128, 255, 116, 1),     # cache one key short of two tiles
+    (10, 2, 128, 128, 77, 0),     # cache exactly one tile, 385 rows, no append
+    (7, 1, 64, 4100, 39, 1),      # group of 7, many splits
 ])
 def test_decode_matches_oracle(shape):
     n_q, n_kv, d, lc, n_new, app = shape
