@@ -19,7 +19,6 @@ from .decode_oracle import (  # noqa: F401
     decode_attention_ref,
     merge_ref,
     stage2_ref,
-    decode_bytes,
 )
 from .scorer_oracle import (  # noqa: F401
     scorer_features,

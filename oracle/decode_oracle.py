@@ -103,10 +103,3 @@ def stage2_ref(q, caches, k_new, v_new, *, scale=None):
     a, lse = merge_ref(np.stack([p[0] for p in parts]), np.stack([p[1] for p in parts]))
     return a, lse, parts
 
-
-def decode_bytes(n_q, n_kv, head_dim, cache_len, n_new, has_new_kv) -> int:
-    """Algorithmic HBM bytes of one host's stage-2 attention: Q, the cache (and
-    the new K/V) read once, the fp32 partial output and LSE written once."""
-    keys = cache_len + (n_new if has_new_kv else 0)
-    return (2 * n_q * n_new * head_dim + 2 * 2 * n_kv * keys * head_dim
-            + 4 * n_q * n_new * head_dim + 4 * n_q * n_new)

@@ -69,8 +69,10 @@ apb_status_t apb_validate_problem(const apb_problem_t* p) {
   const int64_t rows = (int64_t)p->anchor_len + (int64_t)p->host_idx * p->pass_len +
                        (int64_t)p->local_len;
   if (rows > kMaxRows) return APB_ERR_BAD_SHAPE;
-  // Grid size: query tiles of 128 rows times query heads must fit a 1-D grid.
-  const int64_t tiles = ((int64_t)p->anchor_len + p->local_len + 127) / 128 * p->n_q_heads;
+  // Grid size: the attention kernel's query tiles times the query heads must
+  // fit its 1-D grid.
+  const int64_t tile = apb::attention_tile_rows();
+  const int64_t tiles = ((int64_t)p->anchor_len + p->local_len + tile - 1) / tile * p->n_q_heads;
   if (tiles >= (int64_t(1) << 31)) return APB_ERR_BAD_SHAPE;
   if (p->head_dim != 64 && p->head_dim != 128) return APB_ERR_UNSUPPORTED;
   return APB_OK;

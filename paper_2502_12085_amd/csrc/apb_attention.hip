@@ -577,6 +577,8 @@ attn_fwd_kernel(Params p) {
 
 }  // namespace
 
+int attention_tile_rows() { return kBM; }
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
   Params p;
   p.q = a.q; p.k = a.k; p.v = a.v; p.kp = a.kp; p.vp = a.vp; p.o = a.o; p.lse = a.lse;

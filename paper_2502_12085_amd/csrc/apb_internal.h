@@ -110,6 +110,7 @@ struct LayerArgs {
 };
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+int attention_tile_rows();   // query rows per attention workgroup (one grid entry each)
 hipError_t launch_compress(const CompressArgs& a, hipStream_t stream);
 DecodePlan plan_decode(const DecodeArgs& a);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);

@@ -74,12 +74,26 @@ def run_compress(prob, scores, k, v, out_k=None, out_v=None):
     return idx, out_k, out_v
 
 
-def assert_attention_close(o_gpu, lse_gpu, o_ref, lse_ref, what=""):
+# Peaked softmax (a test's softmax_scale of 1.0): an output row is then close
+# to a single value row, |O| reaches max|V| (about 5 for N(0, 1) values), and
+# the arithmetic's own rounding grows with it: O rounded to bf16 (up to 2^-9
+# |O|) plus the probabilities rounded to bf16 for the value product (up to
+# 2^-9 of the weighted |V|, about |O| when one key dominates).  The bar for
+# such cases adds that bound, 2^-8 |O_ref|, to the absolute 2e-2 per element.
+O_REL_PEAKED = 2.0 ** -8
+
+
+def assert_attention_close(o_gpu, lse_gpu, o_ref, lse_ref, what="", o_rel=0.0):
     o_gpu = np.asarray(o_gpu, dtype=np.float64)
     assert np.isfinite(o_gpu).all(), f"{what}: non-finite output"
     err = np.abs(o_gpu - o_ref)
     lerr = np.abs(np.asarray(lse_gpu, dtype=np.float64) - lse_ref)
     say(f"  {what}: O max {err.max():.3e} mean {err.mean():.3e}  LSE max {lerr.max():.3e}")
-    assert err.max() <= O_MAX_ABS, f"{what}: O max-abs {err.max()}"
+    if o_rel:
+        excess = err - (O_MAX_ABS + o_rel * np.abs(o_ref))
+        say(f"  {what}: largest O error over 2e-2 + {o_rel:.3g}|O_ref|: {excess.max():.3e}")
+        assert excess.max() <= 0, f"{what}: O error {err.max()} past 2e-2 + {o_rel}|O_ref|"
+    else:
+        assert err.max() <= O_MAX_ABS, f"{what}: O max-abs {err.max()}"
     assert err.mean() <= O_MEAN_ABS, f"{what}: O mean-abs {err.mean()}"
     assert lerr.max() <= LSE_MAX_ABS, f"{what}: LSE max-abs {lerr.max()}"

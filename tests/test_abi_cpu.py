@@ -56,6 +56,20 @@ def test_validate_problem(kw, code):
     assert apb.lib().apb_validate_problem(ctypes.byref(_prob(**kw))) == code
 
 
+@pytest.mark.parametrize("rows,n_q,code", [
+    # the attention grid is one workgroup per 256-row query tile per query
+    # head and must stay below 2^31 entries
+    ((1 << 30) - 256, 512, 0),  # (2^22 - 1) tiles x 512 heads = 2^31 - 512
+    (1 << 30, 512, 2),          # 2^22 tiles x 512 heads = 2^31
+    ((1 << 30) - 255, 512, 2),  # one row more rounds up to 2^22 tiles
+    ((1 << 30) - 256, 513, 2),
+])
+def test_validate_problem_grid_boundary(rows, n_q, code):
+    p = _prob(n_hosts=1, host_idx=0, anchor_len=0, local_len=rows, pass_len=0,
+              n_q_heads=n_q, n_kv_heads=1, head_dim=128)
+    assert apb.lib().apb_validate_problem(ctypes.byref(p)) == code
+
+
 def test_flops_match_oracle_closed_form():
     for wl in inputs.WORKLOADS.values():
         p = wl.problem
@@ -183,8 +197,10 @@ def test_decode_error_paths():
     assert _dec(p, ws=None) == 1
     assert _dec(p, kc=None) == 1             # cache required when Lc > 0
     assert _dec(p, kn=None) == 1             # new K/V required on the last host
-    assert _dec(_dprob(append_new=0), kn=None, vn=None) != 1
-    assert _dec(_dprob(cache_len=0), kc=None, vc=None) != 1
+    # optional pointers: validation gets past them and stops at the (too
+    # small) workspace, so nothing is launched on the fake addresses
+    assert _dec(_dprob(append_new=0), kn=None, vn=None, ws_bytes=16) == 2
+    assert _dec(_dprob(cache_len=0), kc=None, vc=None, ws_bytes=16) == 2
     assert _dec(p, ws_bytes=16) == 2         # workspace too small
     assert _dec(p, q=DQ + 8) == 4
     assert _dec(p, o=DO + 4) == 4

@@ -14,6 +14,7 @@ import pytest
 import oracle
 from paper_2502_12085_amd import inputs
 from gpu_util import assert_attention_close, dev_bf16, host_bf16_to_f64, need_gpu, say
+import rescale_cases as rc
 
 pytestmark = pytest.mark.gpu
 
@@ -91,6 +92,20 @@ def test_decode_custom_scale_and_determinism():
     o_ref, lse_ref = oracle.decode_attention_ref(case["q"], kc, vc, case["k_new"], case["v_new"],
                                                  scale=0.05)
     assert_attention_close(o1, l1, o_ref, lse_ref, "decode scale 0.05")
+
+
+@pytest.mark.parametrize("shape", [rc.DECODE_ONE_SPLIT["one_wave"][0],
+                                   rc.DECODE_ONE_SPLIT["eight_wave"][0], rc.DECODE_MANY_SPLITS])
+def test_decode_late_max_raise_scale_one(shape):
+    """softmax_scale = 1.0: the running max moves after a split's first block
+    and rescales a non-zero accumulator (CPU replay of the kernels' decision:
+    tests/test_lazy_max_coverage.py); one-wave and eight-wave kernels."""
+    n_q, n_kv, d, lc, n_new, app = shape
+    say(f"[decode scale 1.0] {shape}")
+    q, kc, vc, kn, vn = rc.decode_inputs(shape)
+    o, lse = _run_decode(q, kc, vc, kn, vn, n_q, n_kv, d, scale=rc.SCALE)
+    o_ref, lse_ref = oracle.decode_attention_ref(q, kc, vc, kn, vn, scale=rc.SCALE)
+    assert_attention_close(o, lse, o_ref, lse_ref, f"decode scale 1.0 {shape}")
 
 
 def _run_merge(o_parts, lse_parts):

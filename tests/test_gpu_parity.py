@@ -9,14 +9,16 @@ import dataclasses
 import json
 import math
 import os
+import zlib
 
 import numpy as np
 import pytest
 
 import oracle
 from paper_2502_12085_amd import inputs
-from gpu_util import (assert_attention_close, host_bf16_to_f64, host_bits, need_gpu,
-                      run_attention, run_compress, say, upload, dev_bf16)
+from gpu_util import (O_REL_PEAKED, assert_attention_close, host_bf16_to_f64, host_bits,
+                      need_gpu, run_attention, run_compress, say, upload, dev_bf16)
+import rescale_cases as rc
 
 pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -113,6 +115,35 @@ def test_softmax_scale_argument():
     assert_attention_close(host_bf16_to_f64(o), lse.cpu().numpy(), o_ref, lse_ref, "scale 0.05")
 
 
+@pytest.mark.parametrize("name", list(rc.ATTENTION))
+def test_late_max_raise_scale_one(name):
+    """softmax_scale = 1.0: the running max moves after the first tile and a
+    non-zero O accumulator is rescaled (CPU replay of the kernel's decision:
+    tests/test_lazy_max_coverage.py), every row against the oracle.  The
+    softmax is peaked, so |O| approaches max|V| and the O bar adds the
+    arithmetic's rounding bound (gpu_util.O_REL_PEAKED)."""
+    need_gpu()
+    p, inp = rc.attention_inputs(name)
+    say(f"[attention scale 1.0] {name} {p}")
+    o, lse = run_attention(p, upload(inp), softmax_scale=rc.SCALE)
+    o_ref, lse_ref = oracle.attention_ref(inp["q"], inp["k"], inp["v"], inp["k_pass"],
+                                          inp["v_pass"], anchor_len=p.anchor_len, scale=rc.SCALE)
+    assert_attention_close(host_bf16_to_f64(o), lse.cpu().numpy(), o_ref, lse_ref,
+                           f"{name} scale 1.0", o_rel=O_REL_PEAKED)
+
+
+def test_planted_late_key_default_scale():
+    """A key planted three tiles in along one query: that query's wave raises
+    its max late at the default scale too."""
+    need_gpu()
+    p, inp = rc.attention_inputs("ragged_d128_planted")
+    o, lse = run_attention(p, upload(inp))
+    o_ref, lse_ref = oracle.attention_ref(inp["q"], inp["k"], inp["v"], inp["k_pass"],
+                                          inp["v_pass"], anchor_len=p.anchor_len)
+    assert_attention_close(host_bf16_to_f64(o), lse.cpu().numpy(), o_ref, lse_ref,
+                           "planted late key", o_rel=O_REL_PEAKED)
+
+
 def test_deterministic_and_fully_written():
     torch = need_gpu()
     wl = _wl("llama8b_32k", n_q_heads=8, n_kv_heads=2)
@@ -148,6 +179,12 @@ def test_llama8b_32k_heads_subset_full_rows():
     """The 32K Llama-8B-shaped share: every row of one query head per KV
     group compared element by element."""
     _full_check(_wl("llama8b_32k"), heads=np.array([0, 5, 10, 15, 16, 22, 27, 31]))
+
+
+def test_llama8b_128k_heads_subset_full_rows():
+    """The 128K Llama-8B-shaped share (outlier K channels): every row of one
+    query head per KV group, element by element."""
+    _full_check(_wl("llama8b_128k"), heads=np.array([0, 5, 10, 15, 16, 22, 27, 31]))
 
 
 def test_d64_many_tiles_full_rows():
@@ -211,7 +248,7 @@ def test_compress_bit_exact(name):
                                   "lp_eq_lb", "lp_one", "ragged"])
 def test_compress_edge_cases(case):
     need_gpu()
-    rng = np.random.default_rng(hash(case) % 1000)
+    rng = np.random.default_rng(zlib.crc32(case.encode()))
     lb, lp, d, n_kv, la = 3000, 700, 128, 3, 40
     s = rng.standard_normal((n_kv, lb)).astype(np.float32)
     if case == "ties":
@@ -231,6 +268,35 @@ def test_compress_edge_cases(case):
         lb, lp, d, la = 1037, 333, 64, 7
         s = np.round(rng.standard_normal((n_kv, lb)) * 3).astype(np.float32)
     p = inputs.Problem(4, 1, la, lb, lp, n_kv, n_kv, d)
+    inp = dict(scores=s, k=rng.integers(0, 65536, (n_kv, la + lb, d), dtype=np.uint16),
+               v=rng.integers(0, 65536, (n_kv, la + lb, d), dtype=np.uint16),
+               q=np.zeros((1, 1, 8), np.uint16), k_pass=np.zeros((1, 8), np.uint16),
+               v_pass=np.zeros((1, 8), np.uint16))
+    _check_compress(p, inp, case)
+
+
+@pytest.mark.parametrize("case", ["normal_131072", "zipf_131072", "ties_nan_inf_ragged",
+                                  "lp_near_lb", "lp_one"])
+def test_compress_long_local_blocks(case):
+    """Local blocks past 65536 rows (the paper's 1024K prefill setting over 8
+    hosts has l_b = 131072): the multi-pass selection kernel, bit-exact."""
+    need_gpu()
+    rng = np.random.default_rng(zlib.crc32(case.encode()))
+    n_kv, la, d = 2, 16, 128
+    lb, lp = 131072, 2048
+    if case == "normal_131072":
+        s = rng.standard_normal((n_kv, lb)).astype(np.float32)
+    elif case == "zipf_131072":
+        s = rng.zipf(1.5, (n_kv, lb)).astype(np.float32)
+    else:
+        lb, d = 65536 + 1234, 64
+        pool = np.array([0.0, -0.0, np.nan, np.inf, -np.inf, 1.0, -1.0, 2.5], np.float32)
+        s = np.round(rng.standard_normal((n_kv, lb)) * 2).astype(np.float32)
+        mask = rng.random((n_kv, lb)) < 0.2
+        s[mask] = rng.choice(pool, int(mask.sum()))
+        lp = {"ties_nan_inf_ragged": 20011, "lp_near_lb": lb - 3, "lp_one": 1}[case]
+    p = inputs.Problem(4, 1, la, lb, lp, n_kv, n_kv, d)
+    say(f"[compress long] {case}: Lb {lb} l_p {lp} d {d}")
     inp = dict(scores=s, k=rng.integers(0, 65536, (n_kv, la + lb, d), dtype=np.uint16),
                v=rng.integers(0, 65536, (n_kv, la + lb, d), dtype=np.uint16),
                q=np.zeros((1, 1, 8), np.uint16), k_pass=np.zeros((1, 8), np.uint16),

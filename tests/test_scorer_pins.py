@@ -109,5 +109,33 @@ def test_anchor_rows_are_not_scored_and_structure():
     np.testing.assert_allclose(s3, 3 * s, rtol=1e-13)
 
 
-def test_flops():
-    assert oracle.scorer_flops(32, 8, 128, 16384, 1024) == 2.0 * 16384 * 6144 * 1024 + 2.0 * 16384 * 1024 * 8
+def _brute_force_multiply_adds(n_q, n_kv, d, lb, hidden):
+    """Multiply-adds of scoring ``lb`` local tokens, counted one by one while
+    the two layers are evaluated in plain Python loops (features gathered
+    head by head, as in the brute-force test above)."""
+    rng = np.random.default_rng(10)
+    feats = (n_q + 2 * n_kv) * d
+    x = rng.standard_normal((lb, feats))
+    w1 = rng.standard_normal((hidden, feats))
+    w2 = rng.standard_normal((n_kv, hidden))
+    count = 0
+    for t in range(lb):
+        hid = []
+        for j in range(hidden):
+            z = 0.0
+            for i in range(feats):
+                z += w1[j][i] * x[t][i]
+                count += 1
+            hid.append(z / (1 + math.exp(-z)))
+        for kv in range(n_kv):
+            acc = 0.0
+            for j in range(hidden):
+                acc += w2[kv][j] * hid[j]
+                count += 1
+    return count
+
+
+@pytest.mark.parametrize("shape", [(2, 1, 2, 3, 3), (4, 2, 8, 5, 16), (3, 3, 4, 1, 7)])
+def test_flops_counted_by_brute_force(shape):
+    # two flops per multiply-add, counted in the loops rather than restated
+    assert oracle.scorer_flops(*shape) == 2.0 * _brute_force_multiply_adds(*shape)
