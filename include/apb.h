@@ -24,7 +24,9 @@
  * and the decoding stage that follows the prefill (Alg. 3):
  *   apb_decode_attention one host's exact attention of the new tokens over
  *                        its KV cache, with the LSE;
- *   apb_merge_partials   MergeScore of the hosts' partial results.
+ *   apb_merge_partials   MergeScore of the hosts' partial results;
+ * plus apb_decode_attention_noalloc, the decode call for callers that cannot
+ * allocate (its scratch is the library's own).
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are caller-owned DEVICE memory on the current HIP
@@ -33,7 +35,9 @@
  *     head-major, row-major, head_dim contiguous, densely packed.  bf16
  *     tensors must be 16-byte aligned; fp32 and int32 tensors 4-byte aligned.
  *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
- *     is the default stream), stateless and re-entrant.  No host sync.
+ *     is the default stream), stateless and re-entrant (except
+ *     apb_decode_attention_noalloc, whose calls on one GPU share its scratch).
+ *     No host sync.
  *   - Every argument is validated on the host BEFORE any HIP call; a call
  *     that returns an error has launched nothing and written nothing.
  *   - Index arithmetic is 64-bit; a problem must satisfy
@@ -49,7 +53,7 @@
 extern "C" {
 #endif
 
-#define APB_ABI_VERSION 4
+#define APB_ABI_VERSION 5
 
 typedef enum {
   APB_OK = 0,
@@ -58,7 +62,9 @@ typedef enum {
   APB_ERR_UNSUPPORTED = 3,  /* valid in the paper, not built here (head_dim) */
   APB_ERR_MISALIGNED = 4,   /* a pointer breaks the alignment rule           */
   APB_ERR_HIP = 5,          /* the HIP runtime reported a launch error       */
-  APB_ERR_ALIAS = 6         /* an output overlaps an input                   */
+  APB_ERR_ALIAS = 6,        /* an output overlaps an input                   */
+  APB_ERR_SCRATCH = 7       /* a no-allocation call needs more scratch than
+                               the library holds                             */
 } apb_status_t;
 
 /* One host's share of one attention layer: the inputs of Alg. 2 (l_p, h, H)
@@ -226,6 +232,32 @@ apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t*
                                   const uint16_t* k_new, const uint16_t* v_new,
                                   float* o_part, float* lse_part, float softmax_scale,
                                   void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * apb_decode_attention_noalloc -- apb_decode_attention for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  Same arguments, result and
+ * arithmetic, minus the workspace: the split partials live in a device array
+ * of APB_DECODE_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it
+ * runs on (from the first call on that GPU until the process ends).  The
+ * call allocates nothing and frees nothing.
+ *
+ *   Limit: when the default split plan's partials (n_split * n_q * n_new *
+ *   (d + 1) * 4 bytes) exceed the array, the keys are split into fewer,
+ *   longer parts (results then differ from apb_decode_attention's by
+ *   rounding only); when even one part (n_q * n_new * (d + 1) * 4 bytes)
+ *   does not fit, the call returns APB_ERR_SCRATCH and launches nothing.
+ *   Races: every call on one GPU shares that GPU's array; calls that overlap
+ *   in time on one GPU (other streams, other host threads) race and give
+ *   undefined results.  Calls in one stream are ordered and safe.  The array
+ *   keeps the last call's partials; nothing in it needs to start at zero.
+ */
+#define APB_DECODE_NOALLOC_SCRATCH_BYTES (32ull << 20)
+apb_status_t apb_decode_attention_noalloc(const apb_decode_problem_t* p, const uint16_t* q,
+                                          const uint16_t* k_cache, const uint16_t* v_cache,
+                                          const uint16_t* k_new, const uint16_t* v_new,
+                                          float* o_part, float* lse_part, float softmax_scale,
+                                          void* stream);
 
 /*
  * apb_merge_partials -- MergeScore of Alg. 3: given P partial results

@@ -14,12 +14,14 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libapb.so")
 
 APB_OK = 0
+NOALLOC_SCRATCH_BYTES = 32 << 20  # APB_DECODE_NOALLOC_SCRATCH_BYTES
 STATUS_NAMES = {0: "APB_OK", 1: "APB_ERR_NULL_POINTER", 2: "APB_ERR_BAD_SHAPE",
                 3: "APB_ERR_UNSUPPORTED", 4: "APB_ERR_MISALIGNED", 5: "APB_ERR_HIP",
-                6: "APB_ERR_ALIAS"}
+                6: "APB_ERR_ALIAS", 7: "APB_ERR_SCRATCH"}
 EXPORTED = ("apb_compress_select", "apb_attention_fwd", "apb_validate_problem",
             "apb_attention_flops", "apb_status_string", "apb_last_error", "apb_abi_version",
             "apb_validate_decode", "apb_decode_workspace_size", "apb_decode_attention",
+            "apb_decode_attention_noalloc",
             "apb_merge_partials", "apb_validate_scorer", "apb_scorer_workspace_size",
             "apb_retaining_scores", "apb_validate_layer", "apb_layer_workspace_size",
             "apb_layer_flops", "apb_layer_fwd")
@@ -128,6 +130,9 @@ def lib() -> ctypes.CDLL:
         L.apb_decode_attention.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp,
                                            ctypes.c_uint64, vp]
         L.apb_decode_attention.restype = ctypes.c_int
+        L.apb_decode_attention_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float,
+                                                   vp]
+        L.apb_decode_attention_noalloc.restype = ctypes.c_int
         L.apb_merge_partials.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp, vp,
                                          vp, vp, vp]
         L.apb_merge_partials.restype = ctypes.c_int
@@ -252,6 +257,22 @@ def decode_attention(problem, q, k_cache, v_cache, k_new, v_new, o_part, lse_par
         _ptr(o_part, "o_part", f), _ptr(lse_part, "lse_part", f), float(softmax_scale),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "apb_decode_attention")
+
+
+def decode_attention_noalloc(problem, q, k_cache, v_cache, k_new, v_new, o_part, lse_part,
+                             softmax_scale=0.0, stream=None):
+    """``apb_decode_attention_noalloc``: ``decode_attention`` without a
+    workspace; the library's own per-GPU scratch holds the split partials
+    (``NOALLOC_SCRATCH_BYTES``).  Calls that overlap on one GPU race."""
+    import torch
+    b = _bf16_types()
+    f = (torch.float32,)
+    st = lib().apb_decode_attention_noalloc(
+        ctypes.byref(DecodeProblem.of(problem)), _ptr(q, "q", b), _ptr(k_cache, "k_cache", b),
+        _ptr(v_cache, "v_cache", b), _ptr(k_new, "k_new", b), _ptr(v_new, "v_new", b),
+        _ptr(o_part, "o_part", f), _ptr(lse_part, "lse_part", f), float(softmax_scale),
+        _stream(stream))
+    _check(st, "apb_decode_attention_noalloc")
 
 
 def merge_partials(o_parts, lse_parts, o, lse=None, stream=None):

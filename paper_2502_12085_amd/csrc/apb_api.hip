@@ -8,6 +8,9 @@
 #include "../../include/apb.h"
 #include "apb_internal.h"
 
+static_assert(APB_DECODE_NOALLOC_SCRATCH_BYTES == apb::kDecodeScratchBytes,
+              "the header states the scratch size the library holds");
+
 namespace {
 
 thread_local char g_last_error[256] = "";
@@ -54,6 +57,9 @@ const char* apb_status_string(int status) {
     case APB_ERR_MISALIGNED: return "a pointer is not aligned (bf16: 16 bytes, fp32/int32: 4 bytes)";
     case APB_ERR_HIP: return "the HIP runtime reported an error";
     case APB_ERR_ALIAS: return "an output overlaps an input";
+    case APB_ERR_SCRATCH:
+      return "the call needs more device scratch than the no-allocation entry point holds "
+             "(APB_DECODE_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }
@@ -379,24 +385,21 @@ apb_status_t apb_decode_workspace_size(const apb_decode_problem_t* p, uint64_t* 
   return APB_OK;
 }
 
-apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t* q,
+// Checks shared by the two decode entry points (everything but the
+// workspace), and the kernel arguments of a valid call.
+static apb_status_t decode_checks(const apb_decode_problem_t* p, const uint16_t* q,
                                   const uint16_t* k_cache, const uint16_t* v_cache,
                                   const uint16_t* k_new, const uint16_t* v_new, float* o_part,
-                                  float* lse_part, float softmax_scale, void* workspace,
-                                  uint64_t workspace_bytes, void* stream) {
+                                  float* lse_part, float softmax_scale, apb::DecodeArgs* a) {
   const apb_status_t st = apb_validate_decode(p);
   if (st != APB_OK) return st;
   const bool has_cache = p->cache_len > 0, app = p->append_new == 1;
-  if (!q || !o_part || !lse_part || !workspace) return APB_ERR_NULL_POINTER;
+  if (!q || !o_part || !lse_part) return APB_ERR_NULL_POINTER;
   if (has_cache && (!k_cache || !v_cache)) return APB_ERR_NULL_POINTER;
   if (app && (!k_new || !v_new)) return APB_ERR_NULL_POINTER;
-  if (!aligned(q, 16) || !aligned(o_part, 16) || !aligned(lse_part, 4) || !aligned(workspace, 16))
-    return APB_ERR_MISALIGNED;
+  if (!aligned(q, 16) || !aligned(o_part, 16) || !aligned(lse_part, 4)) return APB_ERR_MISALIGNED;
   if (has_cache && (!aligned(k_cache, 16) || !aligned(v_cache, 16))) return APB_ERR_MISALIGNED;
   if (app && (!aligned(k_new, 16) || !aligned(v_new, 16))) return APB_ERR_MISALIGNED;
-  apb::DecodeArgs a = decode_args(p);
-  const uint64_t need = apb::plan_decode(a).workspace_bytes;
-  if (workspace_bytes < need) return APB_ERR_BAD_SHAPE;
   const int64_t d = p->head_dim, rows = (int64_t)p->n_q_heads * p->n_new;
   const int64_t cache_bytes = has_cache ? (int64_t)p->n_kv_heads * p->cache_len * d * 2 : 0;
   const int64_t new_bytes = app ? (int64_t)p->n_kv_heads * p->n_new * d * 2 : 0;
@@ -404,25 +407,77 @@ apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t*
                        range_of(has_cache ? v_cache : nullptr, cache_bytes),
                        range_of(app ? k_new : nullptr, new_bytes),
                        range_of(app ? v_new : nullptr, new_bytes)};
-  const Range out[3] = {range_of(o_part, rows * d * 4), range_of(lse_part, rows * 4),
-                        range_of(workspace, (int64_t)need)};
+  const Range out[2] = {range_of(o_part, rows * d * 4), range_of(lse_part, rows * 4)};
   for (const Range& r : out)
     for (const Range& i : in)
       if (overlaps(r, i)) return APB_ERR_ALIAS;
-  if (overlaps(out[0], out[1]) || overlaps(out[0], out[2]) || overlaps(out[1], out[2]))
-    return APB_ERR_ALIAS;
+  if (overlaps(out[0], out[1])) return APB_ERR_ALIAS;
 
+  *a = decode_args(p);
   float scale = softmax_scale;
   if (!(scale > 0.f) || !isfinite(scale)) scale = 1.f / sqrtf((float)p->head_dim);
-  a.q = q;
-  a.kc = has_cache ? k_cache : nullptr;
-  a.vc = has_cache ? v_cache : nullptr;
-  a.kn = app ? k_new : nullptr;
-  a.vn = app ? v_new : nullptr;
-  a.o = o_part; a.lse = lse_part;
+  a->q = q;
+  a->kc = has_cache ? k_cache : nullptr;
+  a->vc = has_cache ? v_cache : nullptr;
+  a->kn = app ? k_new : nullptr;
+  a->vn = app ? v_new : nullptr;
+  a->o = o_part; a->lse = lse_part;
+  a->scale_log2 = scale * 1.4426950408889634f;
+  return APB_OK;
+}
+
+apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t* q,
+                                  const uint16_t* k_cache, const uint16_t* v_cache,
+                                  const uint16_t* k_new, const uint16_t* v_new, float* o_part,
+                                  float* lse_part, float softmax_scale, void* workspace,
+                                  uint64_t workspace_bytes, void* stream) {
+  apb::DecodeArgs a;
+  const apb_status_t st =
+      decode_checks(p, q, k_cache, v_cache, k_new, v_new, o_part, lse_part, softmax_scale, &a);
+  if (st != APB_OK) return st;
+  if (!workspace) return APB_ERR_NULL_POINTER;
+  if (!aligned(workspace, 16)) return APB_ERR_MISALIGNED;
+  const apb::DecodePlan pl = apb::plan_decode(a);
+  if (workspace_bytes < pl.workspace_bytes) return APB_ERR_BAD_SHAPE;
+  const int64_t d = p->head_dim, rows = (int64_t)p->n_q_heads * p->n_new;
+  const bool has_cache = p->cache_len > 0, app = p->append_new == 1;
+  const int64_t cache_bytes = has_cache ? (int64_t)p->n_kv_heads * p->cache_len * d * 2 : 0;
+  const int64_t new_bytes = app ? (int64_t)p->n_kv_heads * p->n_new * d * 2 : 0;
+  const Range ws = range_of(workspace, (int64_t)pl.workspace_bytes);
+  const Range others[7] = {range_of(q, rows * d * 2), range_of(a.kc, cache_bytes),
+                           range_of(a.vc, cache_bytes), range_of(a.kn, new_bytes),
+                           range_of(a.vn, new_bytes), range_of(o_part, rows * d * 4),
+                           range_of(lse_part, rows * 4)};
+  for (const Range& r : others)
+    if (overlaps(ws, r)) return APB_ERR_ALIAS;
   a.workspace = static_cast<float*>(workspace);
-  a.scale_log2 = scale * 1.4426950408889634f;
-  const hipError_t e = apb::launch_decode(a, static_cast<hipStream_t>(stream));
+  const hipError_t e = apb::launch_decode(a, pl, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    set_last_error(e);
+    return APB_ERR_HIP;
+  }
+  return APB_OK;
+}
+
+apb_status_t apb_decode_attention_noalloc(const apb_decode_problem_t* p, const uint16_t* q,
+                                          const uint16_t* k_cache, const uint16_t* v_cache,
+                                          const uint16_t* k_new, const uint16_t* v_new,
+                                          float* o_part, float* lse_part, float softmax_scale,
+                                          void* stream) {
+  apb::DecodeArgs a;
+  const apb_status_t st =
+      decode_checks(p, q, k_cache, v_cache, k_new, v_new, o_part, lse_part, softmax_scale, &a);
+  if (st != APB_OK) return st;
+  // the split partials must fit the library's scratch: fewer, longer splits
+  // when the default plan does not, an error when one split does not
+  const apb::DecodePlan pl = apb::plan_decode(a, APB_DECODE_NOALLOC_SCRATCH_BYTES);
+  if (pl.n_split < 1) return APB_ERR_SCRATCH;
+  void* scratch = nullptr;
+  hipError_t e = apb::decode_scratch(&scratch);
+  if (e == hipSuccess) {
+    a.workspace = static_cast<float*>(scratch);
+    e = apb::launch_decode(a, pl, static_cast<hipStream_t>(stream));
+  }
   if (e != hipSuccess) {
     set_last_error(e);
     return APB_ERR_HIP;

@@ -34,6 +34,8 @@
 // with no part left gets A = 0, lse = -inf.
 #include <math.h>
 
+#include <mutex>
+
 #include "apb_internal.h"
 
 namespace apb {
@@ -824,7 +826,7 @@ hipError_t launch_merge_t(int n_parts, int rows, int d, const float* o_parts,
 
 }  // namespace
 
-DecodePlan plan_decode(const DecodeArgs& a) {
+DecodePlan plan_decode(const DecodeArgs& a, uint64_t max_workspace_bytes) {
   DecodePlan pl;
   const int64_t keys = (int64_t)a.Lc + (a.append ? a.n_new : 0);
   const int64_t R = (int64_t)(a.n_q / a.n_kv) * a.n_new;
@@ -842,16 +844,59 @@ DecodePlan plan_decode(const DecodeArgs& a) {
   if (n_split < 1) n_split = 1;
   int64_t bps = nblk > 0 ? (nblk + n_split - 1) / n_split : 0;
   if (bps > 0) n_split = (nblk + bps - 1) / bps;
+  // a workspace limit caps the splits (longer splits, the same kernels)
+  const int64_t rows_total = (int64_t)a.n_q * a.n_new;
+  const uint64_t per_split = (uint64_t)rows_total * (a.head_dim + 1) * 4;
+  if ((uint64_t)n_split * per_split > max_workspace_bytes) {
+    const int64_t cap = (int64_t)(max_workspace_bytes / per_split);
+    if (cap < 1) {
+      pl.n_split = 0;  // does not fit
+      pl.blocks_per_split = 0;
+      pl.row_blocks = (int)n_rb;
+      pl.workspace_bytes = per_split;
+      return pl;
+    }
+    bps = (nblk + cap - 1) / cap;
+    n_split = (nblk + bps - 1) / bps;
+  }
   pl.n_split = (int)n_split;
   pl.blocks_per_split = (int)bps;
   pl.row_blocks = (int)n_rb;
-  const int64_t rows_total = (int64_t)a.n_q * a.n_new;
-  pl.workspace_bytes = (uint64_t)n_split * rows_total * (a.head_dim + 1) * 4;
+  pl.workspace_bytes = (uint64_t)n_split * per_split;
   return pl;
 }
 
-hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
-  const DecodePlan pl = plan_decode(a);
+// Device scratch of the no-allocation entry point: one array per GPU (each
+// device holds its own copy of a __device__ variable), found once per device
+// by its symbol.  In host code `scratch` names a host-side stand-in, never the
+// device memory: only the address from hipGetSymbolAddress is handed to
+// kernels.
+static __device__ __align__(256) float scratch[kDecodeScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t decode_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* addr = nullptr;
+    e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!addr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = addr;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_decode(const DecodeArgs& a, const DecodePlan& pl, hipStream_t stream) {
   DecParams p;
   p.q = a.q; p.kc = a.kc; p.vc = a.vc; p.kn = a.kn; p.vn = a.vn;
   const int64_t rows_total = (int64_t)a.n_q * a.n_new;

@@ -112,8 +112,13 @@ struct LayerArgs {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 int attention_tile_rows();   // query rows per attention workgroup (one grid entry each)
 hipError_t launch_compress(const CompressArgs& a, hipStream_t stream);
-DecodePlan plan_decode(const DecodeArgs& a);
-hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+// max_workspace_bytes caps the splits; a plan with n_split == 0 does not fit.
+DecodePlan plan_decode(const DecodeArgs& a, uint64_t max_workspace_bytes = ~0ull);
+hipError_t launch_decode(const DecodeArgs& a, const DecodePlan& pl, hipStream_t stream);
+// The no-allocation decode call's device scratch on the current device (its
+// address, looked up once per device), kDecodeScratchBytes long.
+constexpr uint64_t kDecodeScratchBytes = uint64_t(32) << 20;
+hipError_t decode_scratch(void** ptr);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
 uint64_t scorer_workspace_bytes(const ScorerArgs& a);
 hipError_t launch_scorer(const ScorerArgs& a, hipStream_t stream);

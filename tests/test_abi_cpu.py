@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == set(apb.EXPORTED)
     for name in declared:
         assert hasattr(L, name), name
-    assert apb.abi_version() == 4
+    assert apb.abi_version() == 5
 
 
 def _prob(**kw):
@@ -83,7 +83,7 @@ def test_flops_match_oracle_closed_form():
 
 def test_status_strings():
     L = apb.lib()
-    for s in range(7):
+    for s in range(8):
         assert L.apb_status_string(s)
     assert L.apb_status_string(99) == b"unknown status"
 
@@ -209,6 +209,40 @@ def test_decode_error_paths():
     assert _dec(p, ws=DKC + 64) == 6
     assert _dec(p, lse=DO + 16) == 6
     assert _dec(_dprob(head_dim=80)) == 3
+
+
+def _dec_na(p, q=DQ, kc=DKC, vc=DVC, kn=DKN, vn=DVN, o=DO, lse=DL):
+    return apb.lib().apb_decode_attention_noalloc(ctypes.byref(p), q, kc, vc, kn, vn, o, lse, 0.0,
+                                                  None)
+
+
+def test_decode_noalloc_error_paths():
+    # every check runs on the host before any HIP call; the calls below all
+    # fail, so nothing is launched on the fake addresses
+    p = _dprob()
+    assert apb.lib().apb_decode_attention_noalloc(None, DQ, DKC, DVC, DKN, DVN, DO, DL, 0.0,
+                                                  None) == 1
+    assert _dec_na(p, q=None) == 1
+    assert _dec_na(p, lse=None) == 1
+    assert _dec_na(p, kc=None) == 1
+    assert _dec_na(p, kn=None) == 1
+    assert _dec_na(p, q=DQ + 8) == 4
+    assert _dec_na(p, o=DO + 4) == 4
+    assert _dec_na(p, o=DQ) == 6
+    assert _dec_na(p, lse=DO + 16) == 6
+    assert _dec_na(_dprob(head_dim=80)) == 3
+    assert _dec_na(_dprob(n_new=0)) == 2
+    # one split's partials (rows * (d + 1) * 4 bytes) beyond the scratch
+    rows_max = apb.NOALLOC_SCRATCH_BYTES // (129 * 4)
+    big = _dprob(n_q_heads=8, n_kv_heads=8, n_new=rows_max // 8 + 1)
+    assert _dec_na(big) == 7
+    assert apb.lib().apb_status_string(7).startswith(b"the call needs more device scratch")
+
+
+def test_decode_noalloc_scratch_constant_matches_header():
+    text = open(os.path.join(ROOT, "include", "apb.h")).read()
+    m = re.search(r"#define APB_DECODE_NOALLOC_SCRATCH_BYTES \((\d+)ull << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == apb.NOALLOC_SCRATCH_BYTES
 
 
 def test_merge_error_paths():
