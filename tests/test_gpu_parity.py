@@ -63,6 +63,8 @@ def test_tiny_every_host(host_idx):
     (3, 1, 1, 1, 1, 1, 1, 128),          # one anchor row, one local row
     (4, 3, 130, 129, 129, 5, 5, 128),    # l_p = Lb, MHA
     (8, 7, 200, 700, 33, 7, 1, 128),     # GQA ratio 7
+    (1, 0, 0, 1000, 0, 4, 2, 128),       # one host, no anchor: plain causal attention over B
+    (4, 0, 0, 300, 300, 2, 1, 64),       # first host, no anchor, l_p = Lb (nothing passed in)
 ])
 def test_ragged_shapes(shape):
     wl = inputs.Workload("ragged", inputs.Problem(*shape))
@@ -156,6 +158,36 @@ def test_deterministic_and_fully_written():
     assert torch.equal(l1.view(torch.int32), l2.view(torch.int32))
 
 
+def test_unaligned_to_256_bytes_and_no_lse():
+    """Operands and outputs 16 bytes (the ABI's minimum) past a 256-byte
+    boundary, and lse = NULL: the same output bits as aligned buffers."""
+    torch = need_gpu()
+    from paper_2502_12085_amd import apb
+    wl = _wl("tiny", host_idx=3)
+    p = wl.problem
+    inp = inputs.make_inputs(wl, 8)
+    dv = upload(inp)
+    o_ref, lse_ref = run_attention(p, dv)
+
+    def shifted(t):
+        flat = torch.empty(t.numel() + 8, dtype=t.dtype, device="cuda")
+        view = flat[8:].view(t.shape)  # 16 bytes past the allocation's start
+        view.copy_(t)
+        return view
+
+    sq, sk, sv = shifted(dv["q"]), shifted(dv["k"]), shifted(dv["v"])
+    skp, svp = shifted(dv["k_pass"]), shifted(dv["v_pass"])
+    assert all(t.data_ptr() % 256 == 16 for t in (sq, sk, sv, skp, svp))
+    o = shifted(torch.full_like(o_ref, float("nan")))
+    apb.attention_fwd(p, sq, sk, sv, skp, svp, o, None)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int16), o_ref.view(torch.int16))
+    assert_attention_close(host_bf16_to_f64(o), lse_ref.cpu().numpy(),
+                           *oracle.attention_ref(inp["q"], inp["k"], inp["v"], inp["k_pass"],
+                                                 inp["v_pass"], anchor_len=p.anchor_len),
+                           "16-byte aligned, no LSE")
+
+
 def test_guard_bands_untouched():
     torch = need_gpu()
     from paper_2502_12085_amd import apb
@@ -204,6 +236,9 @@ def _sample_rows(p, rng, n_random=24):
 
 @pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k", "qwen14b_256k", "yi34b_512k"])
 def test_full_size_sampled_rows(name):
+    """Sampled rows of several heads (segment boundaries, tile edges, the
+    last rows, random rows); at 256K and 512K also every row of the last
+    query head."""
     torch = need_gpu()
     wl = inputs.WORKLOADS[name]
     p = wl.problem
@@ -221,6 +256,14 @@ def test_full_size_sampled_rows(name):
     og = host_bf16_to_f64(o[torch.as_tensor(heads).cuda()][:, torch.as_tensor(rows).cuda()])
     lg = lse[torch.as_tensor(heads).cuda()][:, torch.as_tensor(rows).cuda()].cpu().numpy()
     assert_attention_close(og, lg, o_ref, lse_ref, name)
+    if name in ("qwen14b_256k", "yi34b_512k"):
+        # and every row of the last query head (the last KV group)
+        last = np.array([p.n_q_heads - 1])
+        say(f"  {name}: every row of query head {last[0]}")
+        o_ref, lse_ref = oracle.attention_ref(inp["q"], inp["k"], inp["v"], inp["k_pass"],
+                                              inp["v_pass"], anchor_len=p.anchor_len, heads=last)
+        assert_attention_close(host_bf16_to_f64(o[last[0]])[None], lse[last[0]].cpu().numpy()[None],
+                               o_ref, lse_ref, f"{name} head {last[0]}")
 
 
 # ------------------------------------------------------------- compressor
@@ -302,6 +345,23 @@ def test_compress_long_local_blocks(case):
                q=np.zeros((1, 1, 8), np.uint16), k_pass=np.zeros((1, 8), np.uint16),
                v_pass=np.zeros((1, 8), np.uint16))
     _check_compress(p, inp, case)
+
+
+def test_compress_without_indices():
+    """out_idx = NULL: the gathered rows are the same bits."""
+    torch = need_gpu()
+    from paper_2502_12085_amd import apb
+    wl = inputs.WORKLOADS["llama8b_32k"]
+    p = wl.problem
+    inp = inputs.make_inputs(wl, 9)
+    dv = upload(inp)
+    _, kc, vc = run_compress(p, dv["scores"], dv["k"], dv["v"])
+    k2 = torch.zeros_like(kc)
+    v2 = torch.zeros_like(vc)
+    apb.compress_select(p, dv["scores"], dv["k"], dv["v"], None, k2, v2)
+    torch.cuda.synchronize()
+    assert torch.equal(k2.view(torch.int16), kc.view(torch.int16))
+    assert torch.equal(v2.view(torch.int16), vc.view(torch.int16))
 
 
 @pytest.mark.parametrize("case", ["misaligned_scores", "big_tie_groups"])
