@@ -11,12 +11,18 @@
 //
 // Kernel design (one workgroup = 8 waves = 256 query rows of one query head,
 // one workgroup per CU):
-//  * Each wave owns 32 query rows and computes S^T = K Q^T with
-//    v_mfma_f32_32x32x16_bf16 (keys on the M side, queries on the N side).
-//    In that accumulator layout a lane holds one query and 16 keys of each
-//    32-key block, so the softmax row statistics are lane-local up to one
-//    v_permlane32_swap, and the probabilities are already laid out as the B
-//    operand of O^T = V^T P^T: no LDS round trip for P.
+//  * Each wave owns 32 query rows (two 16-query blocks) and computes S^T =
+//    K Q^T with v_mfma_f32_16x16x32_bf16 (keys on the M side, queries on the
+//    N side); every K operand read feeds both query blocks.  The 16x16x32
+//    shape accumulates 32 products per output per instruction (the 32x32x16
+//    shape 16), so it moves half the fp32 accumulator data per flop; under
+//    this chip's power limit a bf16 matrix load holds a higher clock with it
+//    (measured: 1.87 vs 1.70 GHz on random operands).  In its accumulator
+//    layout a lane holds 4 keys of each 16-key block for one query of each
+//    block, so the softmax row statistics are lane-local up to an exchange
+//    between four lanes (only on the rare max path and at the end), and the
+//    probabilities are already laid out as the B operand of O^T = V^T P^T: no
+//    LDS round trip for P.
 //  * Ping-pong: the waves form two groups of four (one wave of each per
 //    SIMD) that alternate between an MFMA phase (S of the next 128-key tile
 //    and the PV product of the previous one, interleaved) and a softmax
@@ -54,6 +60,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
@@ -64,7 +71,8 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
 constexpr int kBM = kRowsPerWave * kWaves;  // query rows per workgroup
 constexpr int kBN = 128;                           // keys per tile
-constexpr int kKB = kBN / 32;                      // 32-key blocks per tile
+constexpr int kKB = kBN / 16;                      // 16-key MFMA blocks per tile
+constexpr int kNPC = kBN / 32;                     // 32-key chunks per tile (PV k-steps)
 constexpr int kStages = 2;                         // LDS ring depth for K and V tiles
 constexpr int kPD = 2;                             // LDS operand read-ahead (MFMA steps)
 constexpr int kXcds = 8;                    // MI355X: 8 XCDs, workgroups dealt round-robin
@@ -121,21 +129,13 @@ __device__ __forceinline__ const uint16_t* key_row_sel(const Params& p, const ui
   return in_pass ? pass + pass_row * D : loc + loc_row * D;
 }
 
-// Value held by the lane 32 apart (the other half of the wave holds the
-// other 16 keys of the same query in the 32x32 accumulator layout).
-__device__ __forceinline__ float half_swap(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
-                                                  false);
-  const int lane = threadIdx.x & 63;
-  return __uint_as_float(lane < 32 ? r[1] : r[0]);
-}
-
 // LDS tile layouts: row-major [kBN][D] bf16, 16-byte chunk c of row r stored
 // at chunk position c ^ swz(r).
 //  K: swz = r mod (D/8): the 16 rows one ds_read_b128 pass touches hit 16
 //     different chunk positions.
-//  V: swz = 4 * (r mod 4) (D = 128): a transposing read touches 4 rows x 4
-//     chunks, which land on 16 different chunk positions.
+//  V: swz = 4 * (r mod 4) (D = 128): the 16 lanes of a transposing read
+//     touch 4 rows x 32 bytes (two chunks each), which land on 8 different
+//     chunk positions.
 template <int D>
 __device__ __forceinline__ int k_swz(int r) { return r & (D / 8 - 1); }
 template <int D>
@@ -170,11 +170,11 @@ attn_fwd_kernel(Params p) {
   constexpr int PIECES = kBN * D / PIECE_ELEMS;  // pieces per tile per tensor
   constexpr int WP = PIECES / kGroupWaves;       // pieces per wave per tile
   constexpr int KCH = D / 8;                     // 16-byte chunks per key row
-  constexpr int NKC = D / 16;                    // MFMA k-steps over head_dim
-  constexpr int NDB = D / 32;                    // 32-wide blocks of head_dim in O^T
-  constexpr int NQK = kKB * NKC;                 // QK MFMAs per tile
-  constexpr int NPG = kBN / 16;                  // 16-key groups of P (PV k-steps)
-  constexpr int NPV = NPG * NDB;                 // PV MFMAs per tile
+  constexpr int NKD = D / 32;                    // MFMA k-steps over head_dim (QK)
+  constexpr int NDB = D / 16;                    // 16-wide blocks of head_dim in O^T
+  constexpr int NPC = kNPC;                      // 32-key chunks of P (PV k-steps)
+  constexpr int NQK = kKB * NKD;                 // QK operand reads per tile (two MFMAs each)
+  constexpr int NPV = NPC * NDB;                 // PV operand reads per tile (two MFMAs each)
   constexpr int PD = kPD;
   static_assert(PIECES * PIECE_ELEMS == kBN * D && WP * kGroupWaves == PIECES, "tile split");
   static_assert(WP == 4 || WP == 8, "copy groups of four pieces");
@@ -293,86 +293,102 @@ attn_fwd_kernel(Params p) {
   const int w_first = r0 + kRowsPerWave * wave;
   const bool w_valid = w_first < p.M;
   const int w_lo = vis_end(w_first, p.La, p.Lp);  // shortest visible prefix in the wave
-  const int rq = w_first + n;  // this lane's query row
-  const int rq_end = vis_end(rq, p.La, p.Lp);
-
-  // Q^T operand: query rq, head_dim slice 16*kc + 8*h .. +7.
-  bf16x8 qreg[NKC];
-  {
-    const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq, p.M - 1)) * D;
-    const unsigned keep = rq < p.M ? ~0u : 0u;  // rows past the end multiply by zero
+  // 16x16x32 MFMAs: lane (li, lg) is column li of a 16-wide block and holds
+  // rows 4*lg .. 4*lg+3 of its accumulator; a wave's 32 queries are two
+  // 16-query blocks qb.
+  const int li = lane & 15, lg = lane >> 4;
+  int rq[2], rq_end[2];
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) {
-      u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 16 * kc + 8 * h);
-      qreg[kc] = __builtin_bit_cast(bf16x8, raw & keep);
+  for (int qb = 0; qb < 2; ++qb) {
+    rq[qb] = w_first + 16 * qb + li;
+    rq_end[qb] = vis_end(rq[qb], p.La, p.Lp);
+  }
+
+  // Q^T operand (B of S^T = K Q^T): query block qb, d-step kd holds query
+  // rq[qb], dims 32*kd + 8*lg .. +7.
+  bf16x8 qreg[2][NKD];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const uint16_t* qrow = p.q + ((size_t)head * p.M + min(rq[qb], p.M - 1)) * D;
+    const unsigned keep = rq[qb] < p.M ? ~0u : 0u;  // rows past the end multiply by zero
+#pragma unroll
+    for (int kd = 0; kd < NKD; ++kd) {
+      u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 32 * kd + 8 * lg);
+      qreg[qb][kd] = __builtin_bit_cast(bf16x8, raw & keep);
     }
   }
 
-  f32x16 oacc[NDB];
+  f32x4 oacc[NDB][2];  // O^T: 16-dim block db x query block qb
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
-  f32x16 s[kKB];   // S^T of the current tile: one accumulator per 32-key block
-  bf16x8 pb[NPG];  // P of the previous tile: one MFMA B operand per 16-key group
-  float m_run = -INFINITY;  // running max of scaled logits (base-2 units)
-  float l_run = 0.f;        // this lane-half's share of the running sum
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) oacc[db][qb][r] = 0.f;
+  f32x4 s[kKB][2];    // S^T of the current tile: 16-key block kb x query block qb
+  bf16x8 pb[NPC][2];  // P of the previous tile: 32-key chunk x query block (B operands)
+  float m_run[2] = {-INFINITY, -INFINITY};  // running max of scaled logits (base-2 units)
+  float l_run[2] = {0.f, 0.f};              // this lane's share of the running sums
 
   // LDS operands, addressed as (stage base + lane base) ^ (step bits) +
   // immediate, so no per-step address registers stay live across tiles.
-  //  QK step i: k-step kc = i / kKB over head_dim, key block i % kKB; the A
-  //  operand holds K rows (lane n holds key 32*(i%kKB) + n, chunk 2kc + h).
-  //  With the K swizzle, chunk (2kc + h) of row n sits at byte 16*((h ^ n) &
-  //  1) + 16*(n & (KCH-2)) xor 32*kc of the row; the key block is the
+  //  QK step i: d-step kd = i / kKB, key block kb = i % kKB; the A operand
+  //  (16 keys x 32 dims) has lane (li, lg) hold key 16*kb + li, chunk
+  //  4*kd + lg, stored at chunk (4*kd + lg) ^ (li & (KCH-1)): byte
+  //  16*(lg ^ (li & (KCH-1))) xor 64*kd of the row; kb is the immediate.
+  //  PV step i: 32-key chunk kc = i / NDB, dim block db = i % NDB; the B
+  //  operand pb[kc][qb] has lane group lg hold keys 32*kc + 4*lg + 0..3 and
+  //  32*kc + 16 + 4*lg + 0..3 (its S^T accumulator rows, in that order as
+  //  k = 8*lg .. 8*lg + 7), and the A operand (16 dims x 32 keys) comes from
+  //  two transposing reads rd = 0, 1 of those two key runs: in the 16-lane
+  //  group lg, source lane li addresses key row 32*kc + 16*rd + 4*lg + li/4
+  //  at dims 16*db + 4*(li%4) .. +3 (result lane li, slot j gets element
+  //  li%4 of source lane 4j + li/4).  With the V swizzle the dim block lands
+  //  at byte 32*db xor the lane's fixed chunk offset; (kc, rd) is the
   //  immediate.
-  //  PV step i: 16-key group c = i / NDB, dim block db = i % NDB; pb[c] slot
-  //  j of lane half hh holds key 16c + 8*(j/4) + 4*hh + j%4 (the S^T
-  //  accumulator layout), and the A operand (dims x keys) comes from two
-  //  transposing reads of 4 keys each: in a 16-lane group g, source lane sl
-  //  addresses key row 16c + 8*rd + 4*(g/2) + sl/4 at dims 32*db + 16*(g%2)
-  //  + 4*(sl%4) .. +3 (result lane i, slot j gets element i%4 of source
-  //  lane 4j + i/4).  With the V swizzle the dim block lands at byte
-  //  64*(db ^ (row & (NDB-1))) of the row, the rest of the lane's offset is
-  //  fixed, and (c, rd) is the immediate.
-  const uint32_t k_lane = (uint32_t)(n * 2 * D + 16 * ((h ^ n) & 1) + 16 * (n & (KCH - 2)));
+  const uint32_t k_lane = (uint32_t)(li * 2 * D + 16 * (lg ^ (li & (KCH - 1))));
   uint32_t v_lane;
   {
-    const int g = lane >> 4, sl = lane & 15;
-    const int row = 4 * (g >> 1) + (sl >> 2);
-    v_lane = (uint32_t)(row * 2 * D + 64 * (row & (NDB - 1)) + 16 * (2 * (g & 1) + ((sl & 3) >> 1)) +
-                        8 * (sl & 1));
+    const int row = 4 * lg + (li >> 2);
+    const int vs = v_swz<D>(row);
+    v_lane = (uint32_t)(row * 2 * D + 16 * (((li & 3) >> 1) ^ vs) + 8 * (li & 1));
   }
   auto k_operand = [&](uint32_t kb, int i) __attribute__((always_inline)) -> bf16x8 {
-    const uint32_t a = (kb ^ (32u * (uint32_t)(i / kKB))) + (uint32_t)(64 * D * (i % kKB));
+    const uint32_t a = (kb ^ (64u * (uint32_t)(i / kKB))) + (uint32_t)(16 * 2 * D * (i % kKB));
     return *(const lds_bf16x8*)(uintptr_t)a;
   };
   auto v_operand = [&](uint32_t vb, int i) __attribute__((always_inline)) -> bf16x8 {
-    const int c = i / NDB, db = i % NDB;
-    const uint32_t x = vb ^ (64u * (uint32_t)db);
+    const int kc = i / NDB, db = i % NDB;
+    const uint32_t x = vb ^ (32u * (uint32_t)db);
     i16x4 part[2];
 #pragma unroll
     for (int rd = 0; rd < 2; ++rd)
       part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_i16x4*)(uintptr_t)(x + (uint32_t)((16 * c + 8 * rd) * 2 * D)));
+          (lds_i16x4*)(uintptr_t)(x + (uint32_t)((32 * kc + 16 * rd) * 2 * D)));
     return __builtin_bit_cast(
         bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
   };
   auto pv_step = [&](const bf16x8& a, int i) __attribute__((always_inline)) {
-    oacc[i % NDB] =
-        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[i / NDB], oacc[i % NDB], 0, 0, 0);
+    const int kc = i / NDB, db = i % NDB;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+      oacc[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][qb], oacc[db][qb], 0, 0, 0);
   };
   auto qk_step = [&](const bf16x8& a, int i) __attribute__((always_inline)) {
-    const f32x16 zero16 = {};
-    s[i % kKB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[i / kKB],
-                                                         i < kKB ? zero16 : s[i % kKB], 0, 0, 0);
+    const int kd = i / kKB, kb = i % kKB;
+    const f32x4 zero4 = {};
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+      s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qreg[qb][kd],
+                                                          kd == 0 ? zero4 : s[kb][qb], 0, 0, 0);
   };
 
   // MFMA steps.  qk_pv(t) computes S(t) = K(t) Q^T and O += P(t-1) V(t-1),
   // the two streams interleaved step by step with their LDS operands read PD
   // steps ahead into rotating registers; qk_only and pv_only are the first
-  // and last tiles.  The scheduling barriers keep the read-ahead distance
-  // (the compiler would otherwise hoist every read of the tile and run out
-  // of registers).
+  // and last tiles.  Every step is two MFMAs per stream (the two query
+  // blocks share the operand read).  The scheduling barriers keep the
+  // read-ahead distance.
   auto k_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(k_lds[t % kStages]) + k_lane; };
   auto v_stage = [&](int t) __attribute__((always_inline)) { return lds_offset(v_lds[t % kStages]) + v_lane; };
   // copy_v: group A's V(t) copies, issued behind the phase's first operand
@@ -423,78 +439,101 @@ attn_fwd_kernel(Params p) {
     }
   };
 
+  // Row statistics: a query's keys of a tile are spread over the four lane
+  // groups (lanes li, li+16, li+32, li+48); the groups' values meet by
+  // cross-lane exchanges, on the rare max path and once at the end.
+  auto row_sum = [](float x) __attribute__((always_inline)) {
+    x += __shfl_xor(x, 16);
+    return x + __shfl_xor(x, 32);
+  };
+  auto row_max = [](float x) __attribute__((always_inline)) {
+    x = fmaxf(x, __shfl_xor(x, 16));
+    return fmaxf(x, __shfl_xor(x, 32));
+  };
+
   // Softmax of tile t: mask, running max, exp2, row sums, P -> bf16.
   auto softmax = [&](int t) __attribute__((always_inline)) {
     const int c0 = t * kBN;
     if (c0 + kBN > w_lo) {  // tile crosses some row's visible end
 #pragma unroll
-      for (int b = 0; b < kKB; ++b)
+      for (int kb = 0; kb < kKB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int c = c0 + 32 * b + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (c >= rq_end) s[b][r] = -INFINITY;
-        }
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int c = c0 + 16 * kb + 4 * lg + r;
+            if (c >= rq_end[qb]) s[kb][qb][r] = -INFINITY;
+          }
     }
     // Lazy running max without a max pass on the common path: the
     // probabilities are taken against the current (possibly stale) m_run,
-    // and only when some row-half's tile sum exceeds kSumLimit (a logit far
-    // above m_run, or the first tile, where m_run = -inf) does the wave find
-    // the tile max, move m_run up to it, rescale O and l, and redo the tile.
-    // O and l share one m_run per row, and O / l and m_run*ln2 + ln(l) do
-    // not depend on its value.
-    // Each 32-key block is processed in three batches (its FMAs, its exp2,
-    // then its sums and bf16 packing) so that no instruction waits on the
-    // latency of the one before it, and only one block's exponentials are
-    // live at a time.
-    float rs[4];
+    // and only when some lane's tile sum of a row exceeds kSumLimit (a logit
+    // far above m_run, or the first tile, where m_run = -inf) does the wave
+    // find the rows' tile max, move m_run up to it, rescale O and l, and
+    // redo the tile.  O and l share one m_run per row (the four lanes of a
+    // row agree on it), and O / l and m_run*ln2 + ln(l) do not depend on its
+    // value.  Each 32-key chunk is processed in three batches (its FMAs, its
+    // exp2, then its sums and bf16 packing), so that no instruction waits on
+    // the latency of the one before it.
+    float rs[2][2];
     auto exp_tile = [&]() __attribute__((always_inline)) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) rs[j] = 0.f;
+      for (int qb = 0; qb < 2; ++qb) rs[qb][0] = rs[qb][1] = 0.f;
 #pragma unroll
-      for (int b = 0; b < kKB; ++b) {
-        f32x16 e;
+      for (int kc = 0; kc < NPC; ++kc) {
+        f32x4 e[2][2];  // [key block 2kc + h][query block]
 #pragma unroll
-        for (int r = 0; r < 16; ++r) e[r] = fmaf(s[b][r], p.scale_log2, -m_run);
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              e[h][qb][r] = fmaf(s[2 * kc + h][qb][r], p.scale_log2, -m_run[qb]);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(e[r]);
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) e[h][qb][r] = __builtin_amdgcn_exp2f(e[h][qb][r]);
         __builtin_amdgcn_sched_barrier(0);
-        // four independent sum chains, chain j over elements 4j .. 4j+3
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
+        for (int qb = 0; qb < 2; ++qb) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) rs[j] += e[4 * j + k];
+          for (int h = 0; h < 2; ++h)
+            rs[qb][h] += (e[h][qb][0] + e[h][qb][1]) + (e[h][qb][2] + e[h][qb][3]);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) pb[2 * b + (r >> 3)][r & 7] = (__bf16)e[r];
+          for (int r = 0; r < 4; ++r) {
+            pb[kc][qb][r] = (__bf16)e[0][qb][r];
+            pb[kc][qb][4 + r] = (__bf16)e[1][qb][r];
+          }
+        }
       }
     };
     exp_tile();
-    const float l_tile = (rs[0] + rs[1]) + (rs[2] + rs[3]);
-    if (__any(!(l_tile <= kSumLimit))) {
-      float mq[4];  // four independent max chains
+    const float l0 = rs[0][0] + rs[0][1], l1 = rs[1][0] + rs[1][1];
+    if (__any(!(l0 <= kSumLimit) || !(l1 <= kSumLimit))) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mq[j] = fmaxf(s[j][0], s[j][1]);
+      for (int qb = 0; qb < 2; ++qb) {
+        float mq[2] = {s[0][qb][0], s[1][qb][0]};  // two independent max chains
 #pragma unroll
-      for (int r = 2; r < 16; ++r)
+        for (int kb = 0; kb < kKB; ++kb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mq[j] = fmaxf(mq[j], s[j % kKB][r]);
+          for (int r = 0; r < 4; ++r) mq[kb & 1] = fmaxf(mq[kb & 1], s[kb][qb][r]);
+        const float mx = row_max(fmaxf(mq[0], mq[1]));
+        const float m_new = fmaxf(m_run[qb], mx * p.scale_log2);
+        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
 #pragma unroll
-      for (int b = 4; b < kKB; ++b)
+        for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mq[r & 3] = fmaxf(mq[r & 3], s[b][r]);
-      float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-      mx = fmaxf(mx, half_swap(mx));
-      const float m_new = fmaxf(m_run, mx * p.scale_log2);
-      const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+          for (int r = 0; r < 4; ++r) oacc[db][qb][r] *= alpha;
+      }
       exp_tile();
     }
-    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) l_run[qb] += rs[qb][0] + rs[qb][1];
   };
 
   // Tiles a wave's rows cannot see need no branch: the mask sets their
@@ -559,20 +598,25 @@ attn_fwd_kernel(Params p) {
     phase_barrier();
   }
 
-  if (!w_valid || rq >= p.M) return;
-  const float l_tot = l_run + half_swap(l_run);
-  const float inv = 1.f / l_tot;
-  uint16_t* orow = p.o + ((size_t)head * p.M + rq) * D;
+  if (!w_valid) return;
+  float l_tot[2];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int qb = 0; qb < 2; ++qb) l_tot[qb] = row_sum(l_run[qb]);  // every lane takes part
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
+  for (int qb = 0; qb < 2; ++qb) {
+    if (rq[qb] >= p.M) continue;
+    const float inv = 1.f / l_tot[qb];
+    uint16_t* orow = p.o + ((size_t)head * p.M + rq[qb]) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
       bf16x4 w;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = (__bf16)(oacc[db][4 * g + i] * inv);
-      *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
+      for (int r = 0; r < 4; ++r) w[r] = (__bf16)(oacc[db][qb][r] * inv);
+      *reinterpret_cast<bf16x4*>(orow + 16 * db + 4 * lg) = w;
     }
-  if (p.lse && h == 0) p.lse[(size_t)head * p.M + rq] = m_run * 0.69314718055994531f + logf(l_tot);
+    if (p.lse && lg == 0)
+      p.lse[(size_t)head * p.M + rq[qb]] = m_run[qb] * 0.69314718055994531f + logf(l_tot[qb]);
+  }
 }
 
 }  // namespace
