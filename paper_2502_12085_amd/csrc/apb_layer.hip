@@ -8,21 +8,24 @@
 //
 // Matrix products.  Every projection is out[t][f] = sum_k x[t][k] W[f][k]
 // (tokens t, output features f, weights row-major [f][k]).  One kernel
-// template covers them: bf16 MFMA 32x32x16 with fp32 accumulation, output
+// template covers them: bf16 MFMA 16x16x32 with fp32 accumulation, output
 // features on the MFMA M side (the weights are the A operand) and tokens on
 // the N side, a 256 x 256 workgroup tile of 4 waves (2 x 2, each 128
-// features x 128 tokens, one wave per SIMD, accumulators in AGPRs), K steps
-// of 64 whose weight and token slabs are copied HBM -> LDS by
-// global_load_lds_dwordx4 into XOR-swizzled tiles in two stages.  Neither a
+// features x 128 tokens in 64 16 x 16 blocks, one wave per SIMD,
+// accumulators in AGPRs), K steps of 64 whose weight and token slabs are
+// copied HBM -> LDS by global_load_lds_dwordx4 into XOR-swizzled tiles in
+// two stages.  (16x16x32 rather than 32x32x16: the same LDS bytes per flop
+// and half the accumulator traffic, which this power-limited chip turns
+// into clock.)  Neither a
 // copy nor an operand read spends a vector instruction on its address: a
 // copy is a scalar base plus a fixed per-lane offset, a read one XOR of a
 // per-lane base plus an instruction offset.  The step
-// boundary is software-pipelined: at its last 16-deep substep a wave waits
+// boundary is software-pipelined: at its last 32-deep substep a wave waits
 // for its copies of the next step, passes the barrier, and issues that
 // substep's MFMAs with the next step's first operand reads and the copies of
-// the step after it (into the stage just finished) behind them; the last two
-// steps are peeled so the steady-state loop has no branches (the compiler
-// can then count outstanding LDS reads exactly).
+// the step after it (into the stage just finished) spread among them; the
+// last two steps are peeled so the steady-state loop has no branches (the
+// compiler can then count outstanding LDS reads exactly).
 // The token operand is read either row-major [t][k] or head-major
 // [k / dh][t][dh] (the attention output, whose heads are the O projection's
 // K dimension), so no transpose is ever materialised.  Epilogues:
@@ -43,7 +46,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
@@ -139,30 +142,35 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
     }
   };
 
-  // ---- operands: lane (n, h) of an MFMA block reads slab row 32*blk + n,
-  // K elements 16*kc + 8*h .. +7, i.e. chunk 2*kc + h of that row, stored at
-  // slot (2*kc + h) ^ swz(row).  swz(row) = (n >> 1) & 7 for every block, so
-  // the address is (lane base ^ 32*kc) plus a constant for stage and block.
-  const int sw = (n >> 1) & 7;
-  const uint32_t lane_chunk = (uint32_t)(32 * (sw >> 1) + 16 * (h ^ (sw & 1)));
-  const uint32_t a_lane = (uint32_t)((128 * wm + n) * 128) + lane_chunk;
-  const uint32_t b_lane = (uint32_t)((128 * wn + n) * 128) + lane_chunk;
-  // stage st's row bases (the stages are 32 KiB apart, so the XOR with 32*kc
+  // ---- operands (16x16x32 MFMAs): lane (li, lg) of a 16-row block reads
+  // slab row 16*blk + li, K elements 32*kc + 8*lg .. +7, i.e. chunk
+  // 4*kc + lg of that row, stored at slot (4*kc + lg) ^ swz(row).
+  // swz(row) = (li >> 1) & 7 for every block, so the address is (lane base
+  // ^ 64*kc) plus a constant for stage and block.  The 16 rows one 16-lane
+  // pass of ds_read_b128 touches land on 16 distinct bank slots.
+  const int li = lane & 15, lg = lane >> 4;
+  const int sw = (li >> 1) & 7;
+  const uint32_t lane_chunk = (uint32_t)(16 * (lg ^ sw));
+  const uint32_t a_lane = (uint32_t)((128 * wm + li) * 128) + lane_chunk;
+  const uint32_t b_lane = (uint32_t)((128 * wn + li) * 128) + lane_chunk;
+  // stage st's row bases (the stages are 32 KiB apart, so the XOR with 64*kc
   // below touches only the chunk bits)
   auto a_base = [&](int st) __attribute__((always_inline)) { return lds_offset(a_lds[st]) + a_lane; };
   auto b_base = [&](int st) __attribute__((always_inline)) { return lds_offset(b_lds[st]) + b_lane; };
   auto read = [](uint32_t base, int blk, int kc) __attribute__((always_inline)) -> bf16x8 {
-    return *(const lds_bf16x8*)(uintptr_t)((base ^ (32u * (uint32_t)kc)) + 4096u * (uint32_t)blk);
+    return *(const lds_bf16x8*)(uintptr_t)((base ^ (64u * (uint32_t)kc)) + 2048u * (uint32_t)blk);
   };
 
-  f32x16 acc[4][4];
+  // acc[mb][nb]: 16 features x 16 tokens; lane (li, lg) holds features
+  // 4*lg .. 4*lg+3 of token li
+  f32x4 acc[8][8];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
+    for (int nb = 0; nb < 8; ++nb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
-  bf16x8 av[2][4], bv[2][4];
+      for (int r = 0; r < 4; ++r) acc[mb][nb][r] = 0.f;
+  bf16x8 av[2][8], bv[2][8];
 
   // prologue: step 0 copied and visible, step 1's copies in flight, step 0's
   // first operands read
@@ -174,40 +182,46 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
     for (int q = 0; q < 16; ++q) copy(1, 1, q);
   }
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) av[0][mb] = read(a_base(0), mb, 0);
+  for (int mb = 0; mb < 8; ++mb) av[0][mb] = read(a_base(0), mb, 0);
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) bv[0][nb] = read(b_base(0), nb, 0);
+  for (int nb = 0; nb < 8; ++nb) bv[0][nb] = read(b_base(0), nb, 0);
 
-  // One K step in four substeps of 16 MFMAs, each followed by the next
-  // substep's eight operand reads.  NEXT: step kk+1 exists (at the last
-  // substep: wait for its copies, barrier, read its first operands); COPY:
-  // step kk+2 exists (its copies, into the stage this step used).
+  // One K step in two substeps of 64 MFMAs; the odd MFMAs among the first 32
+  // of a substep each carry one of the next substep's 16 operand reads.
+  // NEXT: step kk+1 exists (at the last substep: wait for its copies,
+  // barrier, read its first operands); COPY: step kk+2 exists (its 16
+  // copies, into the stage this step used, ride on every fourth MFMA of the
+  // last substep: issued back to back they stall the wave, and the matrix
+  // core with it, for hundreds of cycles).
   auto step = [&](int kk, auto next_t, auto copy_t) __attribute__((always_inline)) {
     constexpr bool NEXT = decltype(next_t)::value, COPY = decltype(copy_t)::value;
     const int st = kk & 1;
     const uint32_t ab = a_base(st), bb = b_base(st), ab1 = a_base(st ^ 1), bb1 = b_base(st ^ 1);
 #pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
-      const int cur = kc & 1, nxt = cur ^ 1;
-      const bool boundary = kc == 3;
+    for (int kc = 0; kc < 2; ++kc) {
+      const int cur = kc, nxt = kc ^ 1;
+      const bool boundary = kc == 1;
       if (boundary && NEXT) {
         // this wave's copies of step kk+1 have landed and its reads of stage
         // st are done; after the barrier every wave's are
         asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
       }
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int mb = i >> 2, nb = i & 3;
-        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[cur][mb], bv[cur][nb],
+      for (int i = 0; i < 64; ++i) {
+        const int mb = i >> 3, nb = i & 7;
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[cur][mb], bv[cur][nb],
                                                               acc[mb][nb], 0, 0, 0);
-        if (!boundary) {
-          if (i < 4) av[nxt][i] = read(ab, i, kc + 1);
-          else if (i < 8) bv[nxt][i - 4] = read(bb, i - 4, kc + 1);
-        } else if (NEXT) {
-          if (i < 4) av[nxt][i] = read(ab1, i, 0);
-          else if (i < 8) bv[nxt][i - 4] = read(bb1, i - 4, 0);
-          if (COPY) copy(kk + 2, st, i);
+        if (i < 32 && (i & 1) == 1) {
+          const int j = i >> 1;
+          if (!boundary) {
+            if (j < 8) av[nxt][j] = read(ab, j, 1);
+            else bv[nxt][j - 8] = read(bb, j - 8, 1);
+          } else if (NEXT) {
+            if (j < 8) av[nxt][j] = read(ab1, j, 0);
+            else bv[nxt][j - 8] = read(bb1, j - 8, 0);
+          }
         }
+        if (boundary && COPY && ((i & 3) == 0)) copy(kk + 2, st, i >> 2);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -219,60 +233,56 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
   if (kk + 1 < nk) step(kk++, yes, no);
   step(kk, no, no);
 
-  // ---- epilogue.  Lane (n, h), block (mb, nb), element r holds slab row
-  // 128*wm + 32*mb + 8*(r/4) + 4*h + r%4 of token t0 + 128*wn + 32*nb + n;
-  // each group of four r is four consecutive features (one 8-byte store).
+  // ---- epilogue.  Lane (li, lg), block (mb, nb), element r holds slab row
+  // 128*wm + 16*mb + 4*lg + r of token t0 + 128*wn + 16*nb + li: four
+  // consecutive features (one 8-byte store).
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
-    const int t = t0 + 128 * wn + 32 * nb + n;
+  for (int nb = 0; nb < 8; ++nb) {
+    const int t = t0 + 128 * wn + 16 * nb + li;
     if (t >= p.T) continue;
     if constexpr (EPI == kEpiSwiglu) {
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < 4; ++mb) {
+        const int f = f0 + 64 * wm + 16 * mb + 4 * lg;
+        if (f >= p.F) continue;
+        bf16x4 o;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int f = f0 + 64 * wm + 32 * mb + 8 * g + 4 * h;
-          if (f >= p.F) continue;
-          bf16x4 o;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float gt = acc[mb][nb][4 * g + i], up = acc[mb + 2][nb][4 * g + i];
-            o[i] = (__bf16)(gt / (1.f + __expf(-gt)) * up);
-          }
-          *reinterpret_cast<bf16x4*>(p.out + (size_t)t * p.F + f) = o;
+        for (int i = 0; i < 4; ++i) {
+          const float gt = acc[mb][nb][i], up = acc[mb + 4][nb][i];
+          o[i] = (__bf16)(gt / (1.f + __expf(-gt)) * up);
         }
+        *reinterpret_cast<bf16x4*>(p.out + (size_t)t * p.F + f) = o;
+      }
     } else {
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
+      for (int mb = 0; mb < 8; ++mb) {
+        const int f = f0 + 128 * wm + 16 * mb + 4 * lg;
+        if (f >= p.F) continue;
+        float v[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int f = f0 + 128 * wm + 32 * mb + 8 * g + 4 * h;
-          if (f >= p.F) continue;
-          float v[4];
+        for (int i = 0; i < 4; ++i) v[i] = acc[mb][nb][i];
+        uint16_t* dst;
+        if constexpr (EPI == kEpiQkv) {
+          const int head = f / p.dh, j = f - head * p.dh;
+          if (head < p.n_q)
+            dst = p.out + ((size_t)head * p.T + t) * p.dh + j;
+          else if (head < p.n_q + p.n_kv)
+            dst = p.out_k + ((size_t)(head - p.n_q) * p.T + t) * p.dh + j;
+          else
+            dst = p.out_v + ((size_t)(head - p.n_q - p.n_kv) * p.T + t) * p.dh + j;
+        } else {
+          dst = p.out + (size_t)t * p.F + f;
+          if (p.resid) {
+            const bf16x4 rr = *reinterpret_cast<const bf16x4*>(p.resid + (size_t)t * p.F + f);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = acc[mb][nb][4 * g + i];
-          uint16_t* dst;
-          if constexpr (EPI == kEpiQkv) {
-            const int head = f / p.dh, j = f - head * p.dh;
-            if (head < p.n_q)
-              dst = p.out + ((size_t)head * p.T + t) * p.dh + j;
-            else if (head < p.n_q + p.n_kv)
-              dst = p.out_k + ((size_t)(head - p.n_q) * p.T + t) * p.dh + j;
-            else
-              dst = p.out_v + ((size_t)(head - p.n_q - p.n_kv) * p.T + t) * p.dh + j;
-          } else {
-            dst = p.out + (size_t)t * p.F + f;
-            if (p.resid) {
-              const bf16x4 rr = *reinterpret_cast<const bf16x4*>(p.resid + (size_t)t * p.F + f);
-#pragma unroll
-              for (int i = 0; i < 4; ++i) v[i] += (float)rr[i];
-            }
+            for (int i = 0; i < 4; ++i) v[i] += (float)rr[i];
           }
-          bf16x4 o;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) o[i] = (__bf16)v[i];
-          *reinterpret_cast<bf16x4*>(dst) = o;
         }
+        bf16x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (__bf16)v[i];
+        *reinterpret_cast<bf16x4*>(dst) = o;
+      }
     }
   }
 }
