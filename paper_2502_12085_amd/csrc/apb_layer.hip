@@ -6,286 +6,16 @@
 // library's own kernels; this file adds the layer's norms, rotary embedding
 // and matrix products, and sequences the whole layer on one stream.
 //
-// Matrix products.  Every projection is out[t][f] = sum_k x[t][k] W[f][k]
-// (tokens t, output features f, weights row-major [f][k]).  One kernel
-// template covers them: bf16 MFMA 16x16x32 with fp32 accumulation, output
-// features on the MFMA M side (the weights are the A operand) and tokens on
-// the N side, a 256 x 256 workgroup tile of 4 waves (2 x 2, each 128
-// features x 128 tokens in 64 16 x 16 blocks, one wave per SIMD,
-// accumulators in AGPRs), K steps of 64 whose weight and token slabs are
-// copied HBM -> LDS by global_load_lds_dwordx4 into XOR-swizzled tiles in
-// two stages.  (16x16x32 rather than 32x32x16: the same LDS bytes per flop
-// and half the accumulator traffic, which this power-limited chip turns
-// into clock.)  Neither a
-// copy nor an operand read spends a vector instruction on its address: a
-// copy is a scalar base plus a fixed per-lane offset, a read one XOR of a
-// per-lane base plus an instruction offset.  The step
-// boundary is software-pipelined: at its last 32-deep substep a wave waits
-// for its copies of the next step, passes the barrier, and issues that
-// substep's MFMAs with the next step's first operand reads and the copies of
-// the step after it (into the stage just finished) spread among them; the
-// last two steps are peeled so the steady-state loop has no branches (the
-// compiler can then count outstanding LDS reads exactly).
-// The token operand is read either row-major [t][k] or head-major
-// [k / dh][t][dh] (the attention output, whose heads are the O projection's
-// K dimension), so no transpose is ever materialised.  Epilogues:
-//  * row-major bf16 store, plus a residual in fp32 before the rounding;
-//  * head-major Q/K/V store of the QKV projection (feature f is dim f % dh
-//    of head f / dh: Q heads, then K heads, then V heads);
-//  * SwiGLU: each wave's 128 weight rows are 64 gate rows and the 64 up
-//    rows of the same features, so gate and up of one feature sit in the
-//    same lane and register slot and SiLU(gate) * up is formed in registers.
+// Matrix products: the GEMM kernel template of apb_gemm.h.
 #include <math.h>
 
 #include <type_traits>
 
+#include "apb_gemm.h"
 #include "apb_internal.h"
 
 namespace apb {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
-
-constexpr int kBF = 256;        // weight rows (output features) per workgroup
-constexpr int kBT = 256;        // tokens per workgroup
-constexpr int kBK = 64;         // K per step
-constexpr int kGemmThreads = 256;
-constexpr int kPieces = 8;      // 1 KiB copy pieces per slab per wave per step
-constexpr int kTileElems = kBF * kBK;  // = kBT * kBK
-
-enum XMode { kXRowMajor = 0, kXHeadMajor = 1 };
-enum WMode { kWPlain = 0, kWGateUp = 1 };
-enum Epi { kEpiRowMajor = 0, kEpiQkv = 1, kEpiSwiglu = 2 };
-
-struct GemmParams {
-  const uint16_t* x;      // tokens: [T][K] or [K / dh][T][dh]
-  const uint16_t* w;      // [F][K]; the gate matrix for kWGateUp
-  const uint16_t* w_up;   // [F][K] for kWGateUp
-  const uint16_t* resid;  // [T][F] or null (kEpiRowMajor)
-  uint16_t* out;          // [T][F] (kEpiRowMajor, kEpiSwiglu); Q for kEpiQkv
-  uint16_t* out_k;        // kEpiQkv: K [n_kv][T][dh]
-  uint16_t* out_v;        // kEpiQkv: V [n_kv][T][dh]
-  int T, K, F;            // F: output features (I for kWGateUp)
-  int dh;                 // head dim of a head-major operand or output
-  int n_q, n_kv;          // kEpiQkv
-};
-
-__device__ __forceinline__ uint32_t lds_offset(const void* p) {
-  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
-}
-
-// 16-byte chunk c of tile row r (128 bytes) sits at chunk c ^ ((r >> 1) & 7):
-// any 16 consecutive rows, which one 16-lane pass of ds_read_b128 touches,
-// land on 16 distinct 16-byte slots of the 256 bank bytes.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
-
-template <int XM, int WM, int EPI>
-__global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t a_lds[2][kTileElems];  // weight slab
-  __shared__ __attribute__((aligned(16))) uint16_t b_lds[2][kTileElems];  // token slab
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave & 1, wn = wave >> 1;  // feature half, token half
-  const int n = lane & 31, h = lane >> 5;
-  const int t0 = blockIdx.x * kBT;
-  const int f0 = blockIdx.y * (WM == kWGateUp ? kBF / 2 : kBF);
-  const int nk = p.K / kBK;
-
-  // ---- copies: piece j (8 rows x 128 bytes) of each slab; wave w copies
-  // pieces 8w .. 8w+7.  Lane l takes row l/8 of the piece and fetches the
-  // chunk that belongs at slot l%8.  Rows past the last feature or token
-  // repeat it (their results are never stored).  A copy is a scalar base (the
-  // operand's first row for this workgroup, advanced by the K step in scalar
-  // registers) plus a fixed per-lane byte offset: no vector instruction.
-  const int cp_row = lane >> 3, cp_slot = lane & 7;
-  const int x_ld = XM == kXHeadMajor ? p.dh : p.K;  // elements between token rows
-  uint32_t w_off[kPieces], x_off[kPieces];
-#pragma unroll
-  for (int i = 0; i < kPieces; ++i) {
-    const int rho = 8 * (kPieces * wave + i) + cp_row;  // slab row 0..255
-    const int chunk = 8 * (cp_slot ^ swz(rho));
-    int fr = WM == kWGateUp ? f0 + 64 * (rho >> 7) + (rho & 63) : f0 + rho;
-    fr = min(fr, p.F - 1);
-    w_off[i] = 2u * (uint32_t)((fr - f0) * p.K + chunk);
-    const int tr = min(t0 + rho, p.T - 1);
-    x_off[i] = 2u * (uint32_t)((tr - t0) * x_ld + chunk);
-  }
-  const uint16_t* const w_first = p.w + (size_t)f0 * p.K;
-  const uint16_t* const w_up_first = (WM == kWGateUp ? p.w_up : p.w) + (size_t)f0 * p.K;
-  const uint16_t* const x_first = p.x + (size_t)t0 * x_ld;
-  // copy q (0..15) of step kk into stage st: q < 8 weight pieces, else token pieces
-  auto copy = [&](int kk, int st, int q) __attribute__((always_inline)) {
-    const int k0 = kk * kBK;
-    const int i = q & 7;
-    const int j = kPieces * wave + i;
-    if (q < 8) {
-      // gate/up: rows 64..127 of either 128-row half are up-projection rows
-      const uint16_t* base =
-          (WM == kWGateUp && ((kPieces * wave + i) & 15) >= 8 ? w_up_first : w_first) + k0;
-      const uint32_t d = __builtin_amdgcn_readfirstlane(lds_offset(&a_lds[st][j * 512]));
-      asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(w_off[i]), "s"(base),
-                   "s"(d)
-                   : "memory");
-    } else {
-      // head-major tokens: K element k0 is column k0 % dh of head k0 / dh
-      const size_t xoff = XM == kXHeadMajor ? (size_t)(k0 / p.dh) * p.T * p.dh + (k0 % p.dh) : (size_t)k0;
-      const uint16_t* base = x_first + xoff;
-      const uint32_t d = __builtin_amdgcn_readfirstlane(lds_offset(&b_lds[st][j * 512]));
-      asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(x_off[i]), "s"(base),
-                   "s"(d)
-                   : "memory");
-    }
-  };
-
-  // ---- operands (16x16x32 MFMAs): lane (li, lg) of a 16-row block reads
-  // slab row 16*blk + li, K elements 32*kc + 8*lg .. +7, i.e. chunk
-  // 4*kc + lg of that row, stored at slot (4*kc + lg) ^ swz(row).
-  // swz(row) = (li >> 1) & 7 for every block, so the address is (lane base
-  // ^ 64*kc) plus a constant for stage and block.  The 16 rows one 16-lane
-  // pass of ds_read_b128 touches land on 16 distinct bank slots.
-  const int li = lane & 15, lg = lane >> 4;
-  const int sw = (li >> 1) & 7;
-  const uint32_t lane_chunk = (uint32_t)(16 * (lg ^ sw));
-  const uint32_t a_lane = (uint32_t)((128 * wm + li) * 128) + lane_chunk;
-  const uint32_t b_lane = (uint32_t)((128 * wn + li) * 128) + lane_chunk;
-  // stage st's row bases (the stages are 32 KiB apart, so the XOR with 64*kc
-  // below touches only the chunk bits)
-  auto a_base = [&](int st) __attribute__((always_inline)) { return lds_offset(a_lds[st]) + a_lane; };
-  auto b_base = [&](int st) __attribute__((always_inline)) { return lds_offset(b_lds[st]) + b_lane; };
-  auto read = [](uint32_t base, int blk, int kc) __attribute__((always_inline)) -> bf16x8 {
-    return *(const lds_bf16x8*)(uintptr_t)((base ^ (64u * (uint32_t)kc)) + 2048u * (uint32_t)blk);
-  };
-
-  // acc[mb][nb]: 16 features x 16 tokens; lane (li, lg) holds features
-  // 4*lg .. 4*lg+3 of token li
-  f32x4 acc[8][8];
-#pragma unroll
-  for (int mb = 0; mb < 8; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[mb][nb][r] = 0.f;
-  bf16x8 av[2][8], bv[2][8];
-
-  // prologue: step 0 copied and visible, step 1's copies in flight, step 0's
-  // first operands read
-#pragma unroll
-  for (int q = 0; q < 16; ++q) copy(0, 0, q);
-  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-  if (nk > 1) {
-#pragma unroll
-    for (int q = 0; q < 16; ++q) copy(1, 1, q);
-  }
-#pragma unroll
-  for (int mb = 0; mb < 8; ++mb) av[0][mb] = read(a_base(0), mb, 0);
-#pragma unroll
-  for (int nb = 0; nb < 8; ++nb) bv[0][nb] = read(b_base(0), nb, 0);
-
-  // One K step in two substeps of 64 MFMAs; the odd MFMAs among the first 32
-  // of a substep each carry one of the next substep's 16 operand reads.
-  // NEXT: step kk+1 exists (at the last substep: wait for its copies,
-  // barrier, read its first operands); COPY: step kk+2 exists (its 16
-  // copies, into the stage this step used, ride on every fourth MFMA of the
-  // last substep: issued back to back they stall the wave, and the matrix
-  // core with it, for hundreds of cycles).
-  auto step = [&](int kk, auto next_t, auto copy_t) __attribute__((always_inline)) {
-    constexpr bool NEXT = decltype(next_t)::value, COPY = decltype(copy_t)::value;
-    const int st = kk & 1;
-    const uint32_t ab = a_base(st), bb = b_base(st), ab1 = a_base(st ^ 1), bb1 = b_base(st ^ 1);
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-      const int cur = kc, nxt = kc ^ 1;
-      const bool boundary = kc == 1;
-      if (boundary && NEXT) {
-        // this wave's copies of step kk+1 have landed and its reads of stage
-        // st are done; after the barrier every wave's are
-        asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      }
-#pragma unroll
-      for (int i = 0; i < 64; ++i) {
-        const int mb = i >> 3, nb = i & 7;
-        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[cur][mb], bv[cur][nb],
-                                                              acc[mb][nb], 0, 0, 0);
-        if (i < 32 && (i & 1) == 1) {
-          const int j = i >> 1;
-          if (!boundary) {
-            if (j < 8) av[nxt][j] = read(ab, j, 1);
-            else bv[nxt][j - 8] = read(bb, j - 8, 1);
-          } else if (NEXT) {
-            if (j < 8) av[nxt][j] = read(ab1, j, 0);
-            else bv[nxt][j - 8] = read(bb1, j - 8, 0);
-          }
-        }
-        if (boundary && COPY && ((i & 3) == 0)) copy(kk + 2, st, i >> 2);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-  };
-  const std::true_type yes{};
-  const std::false_type no{};
-  int kk = 0;
-  for (; kk + 2 < nk; ++kk) step(kk, yes, yes);
-  if (kk + 1 < nk) step(kk++, yes, no);
-  step(kk, no, no);
-
-  // ---- epilogue.  Lane (li, lg), block (mb, nb), element r holds slab row
-  // 128*wm + 16*mb + 4*lg + r of token t0 + 128*wn + 16*nb + li: four
-  // consecutive features (one 8-byte store).
-#pragma unroll
-  for (int nb = 0; nb < 8; ++nb) {
-    const int t = t0 + 128 * wn + 16 * nb + li;
-    if (t >= p.T) continue;
-    if constexpr (EPI == kEpiSwiglu) {
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        const int f = f0 + 64 * wm + 16 * mb + 4 * lg;
-        if (f >= p.F) continue;
-        bf16x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float gt = acc[mb][nb][i], up = acc[mb + 4][nb][i];
-          o[i] = (__bf16)(gt / (1.f + __expf(-gt)) * up);
-        }
-        *reinterpret_cast<bf16x4*>(p.out + (size_t)t * p.F + f) = o;
-      }
-    } else {
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb) {
-        const int f = f0 + 128 * wm + 16 * mb + 4 * lg;
-        if (f >= p.F) continue;
-        float v[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = acc[mb][nb][i];
-        uint16_t* dst;
-        if constexpr (EPI == kEpiQkv) {
-          const int head = f / p.dh, j = f - head * p.dh;
-          if (head < p.n_q)
-            dst = p.out + ((size_t)head * p.T + t) * p.dh + j;
-          else if (head < p.n_q + p.n_kv)
-            dst = p.out_k + ((size_t)(head - p.n_q) * p.T + t) * p.dh + j;
-          else
-            dst = p.out_v + ((size_t)(head - p.n_q - p.n_kv) * p.T + t) * p.dh + j;
-        } else {
-          dst = p.out + (size_t)t * p.F + f;
-          if (p.resid) {
-            const bf16x4 rr = *reinterpret_cast<const bf16x4*>(p.resid + (size_t)t * p.F + f);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) v[i] += (float)rr[i];
-          }
-        }
-        bf16x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = (__bf16)v[i];
-        *reinterpret_cast<bf16x4*>(dst) = o;
-      }
-    }
-  }
-}
 
 // RMSNorm of one row per workgroup: out = in / sqrt(mean(in^2) + eps) * gain,
 // fp32 arithmetic, bf16 in and out.  D % 8 == 0.
@@ -343,13 +73,6 @@ __global__ void __launch_bounds__(256) rope_kernel(uint16_t* __restrict__ q,
   }
 }
 
-template <int XM, int WM, int EPI>
-hipError_t launch_gemm(const GemmParams& p, hipStream_t stream) {
-  const int per_wg = WM == kWGateUp ? kBF / 2 : kBF;
-  const dim3 grid((unsigned)((p.T + kBT - 1) / kBT), (unsigned)((p.F + per_wg - 1) / per_wg));
-  hipLaunchKernelGGL((gemm_kernel<XM, WM, EPI>), grid, dim3(kGemmThreads), 0, stream, p);
-  return hipGetLastError();
-}
 
 // Workspace carve-up (256-byte aligned pieces).
 struct LayerPlan {
