@@ -86,6 +86,8 @@ struct GemmParams {
   const float* b1;        // [F]
   const float* w2;        // [n_kv][F]
   float* part;            // [F / kBF][n_kv][T] fp32 partial scores per feature block
+  // tile grid (set by launch_gemm): token tiles, feature tiles, 8-tile blocks along tokens
+  int ntx, nfy, nbt;
 };
 
 __device__ __forceinline__ uint32_t lds_offset(const void* p) {
@@ -106,8 +108,17 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;  // feature half, token half
   const int n = lane & 31, h = lane >> 5;
-  const int t0 = blockIdx.x * kBT;
-  const int f0 = blockIdx.y * (WM == kWGateUp ? kBF / 2 : kBF);
+  // Blocked, XCD-aware tile order: workgroup b runs on XCD b % 8, and the 32
+  // consecutive workgroups of one XCD take one block of 4 feature x 8 token
+  // tiles, starting and finishing together, so per K step the XCD's L2
+  // fetches 4 weight and 8 token slabs for 32 workgroups (with the tiles
+  // dealt in grid order the same L2 fetched 1.2-3x the bytes).
+  const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
+  const int blk = (slot >> 5) * 8 + xcd, sb = slot & 31;
+  const int ftile = (blk / p.nbt) * 4 + (sb >> 3), ttile = (blk % p.nbt) * 8 + (sb & 7);
+  if (ftile >= p.nfy || ttile >= p.ntx) return;  // past the grid's edge
+  const int t0 = ttile * kBT;
+  const int f0 = ftile * (WM == kWGateUp ? kBF / 2 : kBF);
   const int nk = p.K / kBK;
 
   // ---- copies: piece j (8 rows x 128 bytes) of each slab; wave w copies
@@ -318,7 +329,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
       const int kv = i / kBT, tl = i % kBT;
       const int t = t0 + tl;
       if (kv < p.n_kv && t < p.T)
-        p.part[((size_t)blockIdx.y * p.n_kv + kv) * p.T + t] =
+        p.part[((size_t)ftile * p.n_kv + kv) * p.T + t] =
             red[kv * kBT + tl] + red[(kScorerMaxKv + kv) * kBT + tl];
     }
     return;
@@ -375,9 +386,13 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
 }
 
 template <int XM, int WM, int EPI>
-hipError_t launch_gemm(const GemmParams& p, hipStream_t stream) {
+hipError_t launch_gemm(GemmParams p, hipStream_t stream) {
   const int per_wg = WM == kWGateUp ? kBF / 2 : kBF;
-  const dim3 grid((unsigned)((p.T + kBT - 1) / kBT), (unsigned)((p.F + per_wg - 1) / per_wg));
+  p.ntx = (p.T + kBT - 1) / kBT;
+  p.nfy = (p.F + per_wg - 1) / per_wg;
+  p.nbt = (p.ntx + 7) / 8;
+  const int nblocks = ((p.nfy + 3) / 4) * p.nbt;  // blocks of 4 x 8 tiles
+  const dim3 grid((unsigned)(256 * ((nblocks + 7) / 8)));
   hipLaunchKernelGGL((gemm_kernel<XM, WM, EPI>), grid, dim3(kGemmThreads), 0, stream, p);
   return hipGetLastError();
 }
