@@ -350,7 +350,7 @@ def bench_scorer(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float =
             "n_kv_heads": p.n_kv_heads, "us": round(us, 2), "flops": flops,
             "tflops": round(tf, 1), "bound": "mfma", "peak": PEAK_BF16_TFLOPS,
             "frac": round(tf / PEAK_BF16_TFLOPS, 4),
-            "kernel": "scorer_gemm_kernel + scorer_reduce_kernel",
+            "kernel": "gemm_kernel<kXQkv, kWPlain, kEpiScorer> + scorer_reduce_kernel",
             "timing": f"median of {steps} back-to-back launches, HIP events", "weights": "synthetic",
             "cpu_baseline": cpu}
 
