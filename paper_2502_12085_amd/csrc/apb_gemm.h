@@ -19,9 +19,11 @@
 // boundary is software-pipelined: at its last 32-deep substep a wave waits
 // for its copies of the next step, passes the barrier, and issues that
 // substep's MFMAs with the next step's first operand reads and the copies of
-// the step after it (into the stage just finished) spread among them; the
-// last two steps are peeled so the steady-state loop has no branches (the
-// compiler can then count outstanding LDS reads exactly).
+// the step after it (into the stage just finished) spread among them (for
+// long K loops the copies start earlier, behind a second barrier that marks
+// the stage free); the last two steps are peeled so the steady-state loop
+// has no branches (the compiler can then count outstanding LDS reads
+// exactly).
 // The token operand is read row-major [t][k], head-major [k / dh][t][dh]
 // (the attention output, whose heads are the O projection's K dimension), or
 // from the head-major Q, K and V tensors as one [Q heads; K heads; V heads]
@@ -99,7 +101,8 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
 // land on 16 distinct 16-byte slots of the 256 bank bytes.
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
-template <int XM, int WM, int EPI>
+// EARLY: the two-barrier step (long K loops), else one barrier per step.
+template <int XM, int WM, int EPI, bool EARLY>
 __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(16))) uint16_t a_lds[2][kTileElems];  // weight slab
   __shared__ __attribute__((aligned(16))) uint16_t b_lds[2][kTileElems];  // token slab
@@ -222,10 +225,16 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
   // One K step in two substeps of 64 MFMAs; the odd MFMAs among the first 32
   // of a substep each carry one of the next substep's 16 operand reads.
   // NEXT: step kk+1 exists (at the last substep: wait for its copies,
-  // barrier, read its first operands); COPY: step kk+2 exists (its 16
-  // copies, into the stage this step used, ride on every fourth MFMA of the
-  // last substep: issued back to back they stall the wave, and the matrix
-  // core with it, for hundreds of cycles).
+  // barrier B, read its first operands); COPY: step kk+2 exists.  Its 16
+  // copies go into the stage this step reads, each on its own MFMA four
+  // apart (issued back to back they stall the wave, and the matrix core with
+  // it, for hundreds of cycles).  That stage is free once every wave has read
+  // the last substep's operands from it.  EARLY marks that point with barrier
+  // A, at MFMA 48 of the first substep, and starts the copies there (4 in
+  // the first substep, 12 in the second), giving them a quarter step more to
+  // land: worth 5% on K loops of hundreds of steps, 1-2% slower on short
+  // ones.  Otherwise the copies start after barrier B, on every fourth MFMA
+  // of the second substep.
   auto step = [&](int kk, auto next_t, auto copy_t) __attribute__((always_inline)) {
     constexpr bool NEXT = decltype(next_t)::value, COPY = decltype(copy_t)::value;
     const int st = kk & 1;
@@ -235,13 +244,21 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
       const int cur = kc, nxt = kc ^ 1;
       const bool boundary = kc == 1;
       if (boundary && NEXT) {
-        // this wave's copies of step kk+1 have landed and its reads of stage
-        // st are done; after the barrier every wave's are
-        asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        // barrier B: this wave's copies of step kk+1 have landed (only the
+        // four copies of step kk+2 issued since barrier A may be
+        // outstanding; copies complete in order); after the barrier every
+        // wave's have
+        if constexpr (EARLY && COPY) asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+        else if constexpr (EARLY) asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
       }
 #pragma unroll
       for (int i = 0; i < 64; ++i) {
         const int mb = i >> 3, nb = i & 7;
+        if (EARLY && !boundary && COPY && i == 48) {
+          // barrier A: every wave's reads of stage st are done
+          asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        }
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[cur][mb], bv[cur][nb],
                                                               acc[mb][nb], 0, 0, 0);
         if (i < 32 && (i & 1) == 1) {
@@ -254,7 +271,14 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
             else bv[nxt][j - 8] = read(bb1, j - 8, 0);
           }
         }
-        if (boundary && COPY && ((i & 3) == 0)) copy(kk + 2, st, i >> 2);
+        if (COPY && (i & 3) == 0) {
+          if constexpr (EARLY) {
+            if (!boundary && i >= 48) copy(kk + 2, st, (i - 48) >> 2);
+            else if (boundary && i < 48) copy(kk + 2, st, 4 + (i >> 2));
+          } else if (boundary) {
+            copy(kk + 2, st, i >> 2);
+          }
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -393,7 +417,10 @@ hipError_t launch_gemm(GemmParams p, hipStream_t stream) {
   p.nbt = (p.ntx + 7) / 8;
   const int nblocks = ((p.nfy + 3) / 4) * p.nbt;  // blocks of 4 x 8 tiles
   const dim3 grid((unsigned)(256 * ((nblocks + 7) / 8)));
-  hipLaunchKernelGGL((gemm_kernel<XM, WM, EPI>), grid, dim3(kGemmThreads), 0, stream, p);
+  if (p.K >= 8192)
+    hipLaunchKernelGGL((gemm_kernel<XM, WM, EPI, true>), grid, dim3(kGemmThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL((gemm_kernel<XM, WM, EPI, false>), grid, dim3(kGemmThreads), 0, stream, p);
   return hipGetLastError();
 }
 
