@@ -125,6 +125,9 @@ def _tiny_variant(name, **kw):
                   n_q_heads=6, n_kv_heads=2, hidden=384, intermediate=320),
     _tiny_variant("d128_gqa4", n_q_heads=8, n_kv_heads=2, head_dim=128, hidden=1024,
                   intermediate=704, anchor_len=0, host_idx=1),
+    # an FFN long enough (K = 8320 in the down product) for the GEMM's
+    # long-K schedule, 65 feature tiles (a partial block of 4) and ragged tokens
+    _tiny_variant("long_ffn", anchor_len=77, local_len=300, intermediate=8320),
 ], ids=lambda lw: lw.name)
 def test_layer_matches_oracle_every_row(lw):
     say(f"[layer] {lw.name}: {lw.problem}, D={lw.hidden}, I={lw.intermediate}")
