@@ -180,8 +180,10 @@ attn_fwd_kernel(Params p) {
   static_assert(WP == 4 || WP == 8, "copy groups of four pieces");
   static_assert(NQK == NPV, "QK and PV step counts match for d in {64, 128}");
 
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kStages][kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kStages][kBN * D];
+  // 256-byte aligned: operand addresses XOR step bits into the low byte of
+  // a stage base plus lane offset
+  __shared__ __attribute__((aligned(256))) uint16_t k_lds[kStages][kBN * D];
+  __shared__ __attribute__((aligned(256))) uint16_t v_lds[kStages][kBN * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;

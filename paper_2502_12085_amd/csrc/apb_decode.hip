@@ -134,8 +134,10 @@ __global__ void __launch_bounds__(64) decode_partial_kernel(DecParams p) {
   static_assert(PIECES == 4 || PIECES == 8, "copy unrolling below");
   constexpr int ROWS_PER_PIECE = 512 / D;
   constexpr int CPW = 2 * PIECES;            // copies per block
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kRing][BK * D];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kRing][BK * D];
+  // 256-byte aligned: operand addresses XOR step bits into the low byte of
+  // a stage base plus lane offset
+  __shared__ __attribute__((aligned(256))) uint16_t k_lds[kRing][BK * D];
+  __shared__ __attribute__((aligned(256))) uint16_t v_lds[kRing][BK * D];
 
   const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
   const int split = blockIdx.x, kvh = blockIdx.y, rb = blockIdx.z;
@@ -402,8 +404,8 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
   constexpr int NPV = NPG * NDB;             // PV MFMAs per tile
   constexpr int PD = 2;                      // operand read-ahead (MFMA steps)
   static_assert(WP * GW == PIECES && WP % 4 == 0 && NQK == NPV, "tile split");
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][BK * D];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][BK * D];
+  __shared__ __attribute__((aligned(256))) uint16_t k_lds[2][BK * D];
+  __shared__ __attribute__((aligned(256))) uint16_t v_lds[2][BK * D];
 
   const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

@@ -4,19 +4,19 @@
 // The library's bf16 matrix products on gfx950, out[t][f] = sum_k x[t][k]
 // W[f][k] (tokens t, output features f, weights row-major [f][k]): the
 // layer's projections (apb_layer.hip) and the first layer of the retaining
-// head (apb_scorer.hip).  One kernel template covers them: bf16 MFMA 16x16x32 with fp32 accumulation, output
-// features on the MFMA M side (the weights are the A operand) and tokens on
-// the N side, a 256 x 256 workgroup tile of 4 waves (2 x 2, each 128
-// features x 128 tokens in 64 16 x 16 blocks, one wave per SIMD,
-// accumulators in AGPRs), K steps of 64 whose weight and token slabs are
-// copied HBM -> LDS by global_load_lds_dwordx4 into XOR-swizzled tiles in
-// two stages.  (16x16x32 rather than 32x32x16: the same LDS bytes per flop
-// and half the accumulator traffic, which this power-limited chip turns
-// into clock.)  Neither a
-// copy nor an operand read spends a vector instruction on its address: a
-// copy is a scalar base plus a fixed per-lane offset, a read one XOR of a
-// per-lane base plus an instruction offset.  The step
-// boundary is software-pipelined: at its last 32-deep substep a wave waits
+// head (apb_scorer.hip).  One kernel template covers them: bf16 MFMA
+// 16x16x32 with fp32 accumulation, output features on the MFMA M side (the
+// weights are the A operand) and tokens on the N side, a 256 x 256
+// workgroup tile of 4 waves (2 x 2, each 128 features x 128 tokens in 64
+// 16 x 16 blocks, one wave per SIMD, accumulators in AGPRs), K steps of 64
+// whose weight and token slabs are copied HBM -> LDS by
+// global_load_lds_dwordx4 into XOR-swizzled tiles in two stages.  (16x16x32
+// rather than 32x32x16: the same LDS bytes per flop and half the
+// accumulator traffic, which this power-limited chip turns into clock.)
+// Neither a copy nor an operand read spends a vector instruction on its
+// address: a copy is a scalar base plus a fixed per-lane offset, a read one
+// XOR of a per-lane base plus an instruction offset.  The step boundary is
+// software-pipelined: at its last 32-deep substep a wave waits
 // for its copies of the next step, passes the barrier, and issues that
 // substep's MFMAs with the next step's first operand reads and the copies of
 // the step after it (into the stage just finished) spread among them (for
@@ -104,13 +104,14 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 // EARLY: the two-barrier step (long K loops), else one barrier per step.
 template <int XM, int WM, int EPI, bool EARLY>
 __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t a_lds[2][kTileElems];  // weight slab
-  __shared__ __attribute__((aligned(16))) uint16_t b_lds[2][kTileElems];  // token slab
+  // 256-byte aligned: operand addresses XOR step bits into the low byte of
+  // a stage base plus lane offset
+  __shared__ __attribute__((aligned(256))) uint16_t a_lds[2][kTileElems];  // weight slab
+  __shared__ __attribute__((aligned(256))) uint16_t b_lds[2][kTileElems];  // token slab
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;  // feature half, token half
-  const int n = lane & 31, h = lane >> 5;
   // Blocked, XCD-aware tile order: workgroup b runs on XCD b % 8, and the 32
   // consecutive workgroups of one XCD take one block of 4 feature x 8 token
   // tiles, starting and finishing together, so per K step the XCD's L2
@@ -132,7 +133,8 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
   // registers) plus a fixed per-lane byte offset: no vector instruction.
   const int cp_row = lane >> 3, cp_slot = lane & 7;
   const int x_ld = XM == kXRowMajor ? p.K : p.dh;  // elements between token rows
-  const int dh_shift = 31 - __builtin_clz((unsigned)p.dh);  // head dims: a power of two
+  // head-major operands: head dims are a power of two (64 or 128)
+  const int dh_shift = XM == kXRowMajor ? 0 : 31 - __builtin_clz((unsigned)p.dh);
   uint32_t w_off[kPieces], x_off[kPieces];
 #pragma unroll
   for (int i = 0; i < kPieces; ++i) {
@@ -161,15 +163,21 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
                    "s"(d)
                    : "memory");
     } else {
-      // head-major tokens: K element k0 is column k0 % dh of head k0 / dh
-      const int head = k0 >> dh_shift, j0 = k0 - (head << dh_shift);
       const uint16_t* base;
-      if constexpr (XM == kXQkv) {
-        const uint16_t* src = head < p.n_q ? p.x : head < p.n_q + p.n_kv ? p.x_k : p.x_v;
-        const int hh = head < p.n_q ? head : head < p.n_q + p.n_kv ? head - p.n_q : head - p.n_q - p.n_kv;
-        base = src + ((size_t)hh * p.x_rows + p.x_row0 + t0) * p.dh + j0;
+      if constexpr (XM == kXRowMajor) {
+        base = x_first + k0;
       } else {
-        base = x_first + (XM == kXHeadMajor ? (size_t)head * p.T * p.dh + j0 : (size_t)k0);
+        // head-major tokens: K element k0 is column k0 % dh of head k0 / dh
+        const int head = k0 >> dh_shift, j0 = k0 - (head << dh_shift);
+        if constexpr (XM == kXQkv) {
+          const uint16_t* src = head < p.n_q ? p.x : head < p.n_q + p.n_kv ? p.x_k : p.x_v;
+          const int hh = head < p.n_q ? head
+                         : head < p.n_q + p.n_kv ? head - p.n_q
+                                                 : head - p.n_q - p.n_kv;
+          base = src + ((size_t)hh * p.x_rows + p.x_row0 + t0) * p.dh + j0;
+        } else {
+          base = x_first + (size_t)head * p.T * p.dh + j0;
+        }
       }
       const uint32_t d = __builtin_amdgcn_readfirstlane(lds_offset(&b_lds[st][j * 512]));
       asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(x_off[i]), "s"(base),
