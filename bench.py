@@ -115,6 +115,61 @@ def busy_ahead(stream, ms: float = 20.0) -> None:
     torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
 
 
+def sample_power(launch, seconds: float = 2.0) -> dict:
+    """Socket power and shader clock while `launch` (one attention call) runs
+    back to back: about `seconds` of launches are queued, and the vendor's
+    SMI tool is read while they run.  Context for the roofline fraction (the
+    chip's clock under a matrix load is set by its power cap); values are
+    None where the tool is missing or prints something else."""
+    import re
+    import shutil
+    import subprocess
+    import torch
+
+    def run(cmd):
+        try:
+            return subprocess.run(cmd, capture_output=True, text=True, timeout=20).stdout
+        except (OSError, subprocess.SubprocessError):
+            return ""
+
+    out = {"during": "back-to-back launches of the attention kernel above",
+           "socket_power_w": None, "power_cap_w": None, "gfx_clk_mhz": None}
+    smi = shutil.which("amd-smi") or "/opt/rocm/bin/amd-smi"
+    rsmi = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    launch()
+    e1.record()
+    torch.cuda.synchronize()
+    n = max(1, int(seconds / max(e0.elapsed_time(e1) * 1e-3, 1e-4)))
+    for _ in range(n):
+        launch()
+    time.sleep(min(0.5, seconds / 4))
+    text = run([smi, "metric", "-p", "-c"]) if os.path.exists(smi) else ""
+    torch.cuda.synchronize()
+    m = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", text)
+    if m:
+        out["socket_power_w"] = float(m.group(1))
+    clks, section = [], ""
+    for line in text.splitlines():
+        h = re.match(r"\s*([A-Z]+_[0-9]+):\s*$", line)
+        if h:
+            section = h.group(1)
+            continue
+        c = re.match(r"\s*CLK:\s*([0-9]+)\s*MHz", line)
+        if c and section.startswith("GFX_"):
+            clks.append(int(c.group(1)))
+    if clks:
+        out["gfx_clk_mhz"] = clks  # one per XCD
+    cap = run([rsmi, "--showmaxpower"]) if os.path.exists(rsmi) else ""
+    m = re.search(r"Max Graphics Package Power \(W\):\s*([0-9.]+)", cap)
+    if m:
+        out["power_cap_w"] = float(m.group(1))
+    out["launches"] = n + 1
+    out["tools"] = "amd-smi metric -p -c; rocm-smi --showmaxpower"
+    return out
+
+
 def bench_mfma_ceiling(steps: int, seed: int = 0) -> dict:
     """Matrix-core ceiling on this chip: the probe library's back-to-back
     32x32x16 bf16 MFMA loop on random N(0,1) operands (one workgroup of 8
@@ -496,6 +551,8 @@ def main():
                     help="skip the matrix-core ceiling probe")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip timing the other workloads (tiny, 32K, 256K, 512K)")
+    ap.add_argument("--no-power", action="store_true",
+                    help="skip reading socket power and shader clock under the attention kernel")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (for scaling "
                          "the HBM byte counters) and exit")
@@ -645,6 +702,9 @@ def main():
                           "note": "8xA800 per-block breakdown at 128K; another machine",
                           "headline_speedups": PAPER_SPEEDUPS},
     }
+    if not args.no_power:
+        result["power"] = sample_power(
+            lambda: apb.attention_fwd(p, q, k, v, kbuf, vbuf, o, lse, 0.0, stream))
     if not args.no_ceiling:
         ceil = bench_mfma_ceiling(max(args.steps // 2, 5))
         ceil["attention_frac_of_ceiling"] = round(achieved / ceil["tflops"], 4)
