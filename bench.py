@@ -115,14 +115,20 @@ def busy_ahead(stream, ms: float = 20.0) -> None:
     torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
 
 
-def sample_power(launch, seconds: float = 2.0) -> dict:
+def sample_power(launch, seconds: float = 3.0) -> dict:
     """Socket power and shader clock while `launch` (one attention call) runs
-    back to back: about `seconds` of launches are queued, and the vendor's
-    SMI tool is read while they run.  Context for the roofline fraction (the
-    chip's clock under a matrix load is set by its power cap); values are
-    None where the tool is missing or prints something else."""
+    back to back: about `seconds` of launches are queued and the vendor's SMI
+    tool is read every quarter second while they run.  `samples` holds each
+    reading (seconds since the queue started, socket watts, mean XCD clock in
+    MHz); `socket_power_w` and `gfx_clk_mhz` (one per XCD) come from the
+    readings taken after the first second, while the chip was still busy
+    (the power manager ramps the clock up from idle over a fraction of a
+    second).  Context for the roofline fraction: the chip's clock under a
+    matrix load is set by its power cap.  Values are None where the tool is
+    missing or prints something else."""
     import re
     import shutil
+    import statistics
     import subprocess
     import torch
 
@@ -132,40 +138,57 @@ def sample_power(launch, seconds: float = 2.0) -> dict:
         except (OSError, subprocess.SubprocessError):
             return ""
 
+    def parse(text):
+        m = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", text)
+        clks, section = [], ""
+        for line in text.splitlines():
+            h = re.match(r"\s*([A-Z]+_[0-9]+):\s*$", line)
+            if h:
+                section = h.group(1)
+                continue
+            c = re.match(r"\s*CLK:\s*([0-9]+)\s*MHz", line)
+            if c and section.startswith("GFX_"):
+                clks.append(int(c.group(1)))
+        return (float(m.group(1)) if m else None), clks
+
     out = {"during": "back-to-back launches of the attention kernel above",
-           "socket_power_w": None, "power_cap_w": None, "gfx_clk_mhz": None}
+           "socket_power_w": None, "power_cap_w": None, "gfx_clk_mhz": None, "samples": []}
     smi = shutil.which("amd-smi") or "/opt/rocm/bin/amd-smi"
     rsmi = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
+    if not os.path.exists(smi):
+        return out
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     launch()
     e1.record()
     torch.cuda.synchronize()
     n = max(1, int(seconds / max(e0.elapsed_time(e1) * 1e-3, 1e-4)))
+    done = torch.cuda.Event()
+    t0 = time.perf_counter()
     for _ in range(n):
         launch()
-    time.sleep(min(0.5, seconds / 4))
-    text = run([smi, "metric", "-p", "-c"]) if os.path.exists(smi) else ""
+    done.record()
+    steady = []
+    while True:
+        time.sleep(0.25)
+        watts, clks = parse(run([smi, "metric", "-p", "-c"]))
+        t = time.perf_counter() - t0
+        busy = not done.query()
+        if not busy:
+            break
+        mean_clk = round(sum(clks) / len(clks)) if clks else None
+        out["samples"].append([round(t, 2), watts, mean_clk])
+        if t >= 1.0 and watts is not None:
+            steady.append((watts, clks))
     torch.cuda.synchronize()
-    m = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", text)
-    if m:
-        out["socket_power_w"] = float(m.group(1))
-    clks, section = [], ""
-    for line in text.splitlines():
-        h = re.match(r"\s*([A-Z]+_[0-9]+):\s*$", line)
-        if h:
-            section = h.group(1)
-            continue
-        c = re.match(r"\s*CLK:\s*([0-9]+)\s*MHz", line)
-        if c and section.startswith("GFX_"):
-            clks.append(int(c.group(1)))
-    if clks:
-        out["gfx_clk_mhz"] = clks  # one per XCD
+    if steady:
+        out["socket_power_w"] = statistics.median(w for w, _ in steady)
+        out["gfx_clk_mhz"] = steady[-1][1] or None
     cap = run([rsmi, "--showmaxpower"]) if os.path.exists(rsmi) else ""
     m = re.search(r"Max Graphics Package Power \(W\):\s*([0-9.]+)", cap)
     if m:
         out["power_cap_w"] = float(m.group(1))
-    out["launches"] = n + 1
+    out["launches"] = n
     out["tools"] = "amd-smi metric -p -c; rocm-smi --showmaxpower"
     return out
 
