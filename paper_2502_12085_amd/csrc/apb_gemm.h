@@ -330,8 +330,10 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
         const float bias = b1_lds[u];
 #pragma unroll
         for (int nb = 0; nb < 8; ++nb) {
+          // SiLU with the hardware reciprocal (within 1 ulp) instead of an
+          // IEEE division, about ten instructions per element
           const float z = acc[mb][nb][r] + bias;
-          const float a = z / (1.f + __expf(-z));
+          const float a = z * __builtin_amdgcn_rcpf(1.f + __expf(-z));
 #pragma unroll
           for (int kv = 0; kv < 4; ++kv) {
             part[nb][kv] = fmaf(a, wa[kv], part[nb][kv]);
