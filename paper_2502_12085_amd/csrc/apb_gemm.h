@@ -381,7 +381,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmParams p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float gt = acc[mb][nb][i], up = acc[mb + 4][nb][i];
-          o[i] = (__bf16)(gt / (1.f + __expf(-gt)) * up);
+          o[i] = (__bf16)(gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up);  // SiLU(gate) * up
         }
         *reinterpret_cast<bf16x4*>(p.out + (size_t)t * p.F + f) = o;
       }
