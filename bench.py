@@ -115,6 +115,30 @@ def busy_ahead(stream, ms: float = 20.0) -> None:
     torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
 
 
+def parse_smi_metric(text: str):
+    """Socket watts and the per-XCD shader clocks (MHz) from the text of
+    `amd-smi metric -p -c` for one GPU: (None, []) where it prints neither."""
+    import re
+    m = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", text)
+    clks, section = [], ""
+    for line in text.splitlines():
+        h = re.match(r"\s*([A-Z]+_[0-9]+):\s*$", line)
+        if h:
+            section = h.group(1)
+            continue
+        c = re.match(r"\s*CLK:\s*([0-9]+)\s*MHz", line)
+        if c and section.startswith("GFX_"):
+            clks.append(int(c.group(1)))
+    return (float(m.group(1)) if m else None), clks
+
+
+def parse_power_cap(text: str):
+    """The package power cap (W) from `rocm-smi --showmaxpower`, or None."""
+    import re
+    m = re.search(r"Max Graphics Package Power \(W\):\s*([0-9.]+)", text)
+    return float(m.group(1)) if m else None
+
+
 def sample_power(launch, seconds: float = 3.0) -> dict:
     """Socket power and shader clock while `launch` (one attention call) runs
     back to back: about `seconds` of launches are queued and the vendor's SMI
@@ -126,7 +150,6 @@ def sample_power(launch, seconds: float = 3.0) -> dict:
     second).  Context for the roofline fraction: the chip's clock under a
     matrix load is set by its power cap.  Values are None where the tool is
     missing or prints something else."""
-    import re
     import shutil
     import statistics
     import subprocess
@@ -137,19 +160,6 @@ def sample_power(launch, seconds: float = 3.0) -> dict:
             return subprocess.run(cmd, capture_output=True, text=True, timeout=20).stdout
         except (OSError, subprocess.SubprocessError):
             return ""
-
-    def parse(text):
-        m = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", text)
-        clks, section = [], ""
-        for line in text.splitlines():
-            h = re.match(r"\s*([A-Z]+_[0-9]+):\s*$", line)
-            if h:
-                section = h.group(1)
-                continue
-            c = re.match(r"\s*CLK:\s*([0-9]+)\s*MHz", line)
-            if c and section.startswith("GFX_"):
-                clks.append(int(c.group(1)))
-        return (float(m.group(1)) if m else None), clks
 
     out = {"during": "back-to-back launches of the attention kernel above",
            "socket_power_w": None, "power_cap_w": None, "gfx_clk_mhz": None, "samples": []}
@@ -171,7 +181,7 @@ def sample_power(launch, seconds: float = 3.0) -> dict:
     steady = []
     while True:
         time.sleep(0.25)
-        watts, clks = parse(run([smi, "metric", "-p", "-c"]))
+        watts, clks = parse_smi_metric(run([smi, "metric", "-p", "-c"]))
         t = time.perf_counter() - t0
         busy = not done.query()
         if not busy:
@@ -185,9 +195,7 @@ def sample_power(launch, seconds: float = 3.0) -> dict:
         out["socket_power_w"] = statistics.median(w for w, _ in steady)
         out["gfx_clk_mhz"] = steady[-1][1] or None
     cap = run([rsmi, "--showmaxpower"]) if os.path.exists(rsmi) else ""
-    m = re.search(r"Max Graphics Package Power \(W\):\s*([0-9.]+)", cap)
-    if m:
-        out["power_cap_w"] = float(m.group(1))
+    out["power_cap_w"] = parse_power_cap(cap)
     out["launches"] = n
     out["tools"] = "amd-smi metric -p -c; rocm-smi --showmaxpower"
     return out
