@@ -225,7 +225,10 @@ apb_status_t apb_decode_workspace_size(const apb_decode_problem_t* p, uint64_t* 
  *                   call overwrites it (calls that overlap in time must not
  *                   share one).  The library allocates nothing.
  * Arithmetic: bf16 inputs, fp32 dot products and softmax, probabilities
- * rounded to bf16 for the value product, fp32 accumulation and output.
+ * rounded to bf16 for the value product, fp32 accumulation and output.  The
+ * key range is split over workgroups whose normalised partials the call
+ * merges: in fp32, or, when a KV head has 128 or more rows, in fp16 scaled
+ * per row by a power of two (each value within 2^-11 of its row's largest).
  */
 apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t* q,
                                   const uint16_t* k_cache, const uint16_t* v_cache,
@@ -242,17 +245,18 @@ apb_status_t apb_decode_attention(const apb_decode_problem_t* p, const uint16_t*
  * runs on (from the first call on that GPU until the process ends).  The
  * call allocates nothing and frees nothing.
  *
- *   Limit: when the default split plan's partials (n_split * n_q * n_new *
- *   (d + 1) * 4 bytes) exceed the array, the keys are split into fewer,
- *   longer parts (results then differ from apb_decode_attention's by
- *   rounding only); when even one part (n_q * n_new * (d + 1) * 4 bytes)
- *   does not fit, the call returns APB_ERR_SCRATCH and launches nothing.
+ *   Limit: when the default split plan's partials exceed the array, the
+ *   keys are split into fewer, longer parts (results then differ from
+ *   apb_decode_attention's by rounding only); when even one part does not
+ *   fit, the call returns APB_ERR_SCRATCH and launches nothing.  A part is
+ *   n_q * n_new rows of (d + 1) * 4 bytes, or of 2 * d + 8 bytes when a KV
+ *   head has 128 or more rows ((n_q / n_kv) * n_new >= 128).
  *   Races: every call on one GPU shares that GPU's array; calls that overlap
  *   in time on one GPU (other streams, other host threads) race and give
  *   undefined results.  Calls in one stream are ordered and safe.  The array
  *   keeps the last call's partials; nothing in it needs to start at zero.
  */
-#define APB_DECODE_NOALLOC_SCRATCH_BYTES (32ull << 20)
+#define APB_DECODE_NOALLOC_SCRATCH_BYTES (16ull << 20)
 apb_status_t apb_decode_attention_noalloc(const apb_decode_problem_t* p, const uint16_t* q,
                                           const uint16_t* k_cache, const uint16_t* v_cache,
                                           const uint16_t* k_new, const uint16_t* v_new,

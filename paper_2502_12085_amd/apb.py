@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libapb.so")
 
 APB_OK = 0
-NOALLOC_SCRATCH_BYTES = 32 << 20  # APB_DECODE_NOALLOC_SCRATCH_BYTES
+NOALLOC_SCRATCH_BYTES = 16 << 20  # APB_DECODE_NOALLOC_SCRATCH_BYTES
 STATUS_NAMES = {0: "APB_OK", 1: "APB_ERR_NULL_POINTER", 2: "APB_ERR_BAD_SHAPE",
                 3: "APB_ERR_UNSUPPORTED", 4: "APB_ERR_MISALIGNED", 5: "APB_ERR_HIP",
                 6: "APB_ERR_ALIAS", 7: "APB_ERR_SCRATCH"}

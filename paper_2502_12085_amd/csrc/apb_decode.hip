@@ -10,8 +10,11 @@
 // once and used by at most g * n_new rows), so the key range is split over
 // many workgroups (flash-decoding): workgroup (s, kv, rb) runs an online
 // softmax over its share of the keys for its rows and writes its normalised
-// partial (O / l, lse) in fp32 to a caller-provided workspace; the merge
-// kernel then combines the splits into the host's partial.  Few rows per KV
+// partial (O / l, lse) to a caller-provided workspace; the merge kernel then
+// combines the splits into the host's partial.  One-wave workgroups write the
+// partial O in fp32; eight-wave ones, whose 256 rows per split make the
+// partials a third of the step's bytes, write it in fp16 against a per-row
+// power-of-two scale (every value within 2^-11 of the row's largest).  Few rows per KV
 // head (one generated token): one-wave workgroups of one 32-row block each.
 // Many rows (the question tokens): eight-wave workgroups that share each
 // 128-key K/V tile among 256 rows and alternate MFMA and softmax phases
@@ -45,6 +48,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
@@ -61,8 +65,10 @@ struct DecParams {
   const uint16_t* vc;
   const uint16_t* kn;
   const uint16_t* vn;
-  float* part_o;    // [n_split][n_q * n_new][d]
-  float* part_lse;  // [n_split][n_q * n_new]
+  float* part_o;        // [n_split][n_q * n_new][d] fp32 (one-wave kernel)
+  uint16_t* part_h;     // [n_split][n_q * n_new][d] fp16 (eight-wave kernel)
+  float* part_scale;    // [n_split][n_q * n_new]: part_h row r is O / part_scale[r]
+  float* part_lse;      // [n_split][n_q * n_new]
   int Lc, n_new, append, n_kv, R, rows_total, blocks_per_split;
   float scale_log2;
 };
@@ -715,19 +721,35 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
   if (!row_ok) return;
   const float l_tot = l_run + half_swap(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  float* orow = p.part_o + ((size_t)split * p.rows_total + grow) * D;
+  // fp16 partial: the row's values (this lane and its partner in the other
+  // half hold 64 dims each) divided by 2^e, e the exponent of the row's
+  // largest magnitude, so every scaled value lies in (-1, 1); the division is
+  // exact and the rounding to fp16 is within 2^-11 of the largest value
+  float mx = 0.f;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      oacc[db][j] *= inv;
+      mx = fmaxf(mx, fabsf(oacc[db][j]));
+    }
+  mx = fmaxf(mx, half_swap(mx));
+  const int e = __builtin_amdgcn_frexp_expf(mx);  // 0 for an all-zero row
+  uint16_t* hrow = p.part_h + ((size_t)split * p.rows_total + grow) * D;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      f32x4 w;
+      f16x4 w;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = oacc[db][4 * g + i] * inv;
-      *reinterpret_cast<f32x4*>(orow + 32 * db + 8 * g + 4 * h) = w;
+      for (int i = 0; i < 4; ++i) w[i] = (_Float16)__builtin_amdgcn_ldexpf(oacc[db][4 * g + i], -e);
+      *reinterpret_cast<f16x4*>(hrow + 32 * db + 8 * g + 4 * h) = w;
     }
-  if (h == 0)
-    p.part_lse[(size_t)split * p.rows_total + grow] =
-        l_tot > 0.f ? m_run * 0.69314718055994531f + logf(l_tot) : -INFINITY;
+  if (h == 0) {
+    const size_t r = (size_t)split * p.rows_total + grow;
+    p.part_lse[r] = l_tot > 0.f ? m_run * 0.69314718055994531f + logf(l_tot) : -INFINITY;
+    p.part_scale[r] = __builtin_amdgcn_ldexpf(1.f, e);
+  }
 }
 
 // MergeScore over n_parts partial results of `rows` rows: one workgroup per
@@ -736,11 +758,24 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
 // parts (the splits of one decode call) and few parts with many rows (the
 // hosts of a decoding step) keep loads in flight; the groups' sums meet in
 // LDS.  THREADS = 1024 when there are few rows and many parts.
-template <typename OutT, int THREADS>
+// Four consecutive values of a part's row as fp32.
+__device__ __forceinline__ f32x4 load_part4(const float* q) {
+  return *reinterpret_cast<const f32x4*>(q);
+}
+__device__ __forceinline__ f32x4 load_part4(const _Float16* q) {
+  const f16x4 v = *reinterpret_cast<const f16x4*>(q);
+  return f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
+
+// PartT: float parts, or _Float16 parts whose row r of part q is O divided
+// by scale_parts[q * rows + r].
+template <typename OutT, int THREADS, typename PartT>
 __global__ void __launch_bounds__(THREADS) merge_kernel(int n_parts, int rows, int d,
-                                                        const float* __restrict__ o_parts,
+                                                        const PartT* __restrict__ o_parts,
+                                                        const float* __restrict__ scale_parts,
                                                         const float* __restrict__ lse_parts,
                                                         OutT* __restrict__ o, float* __restrict__ lse) {
+  constexpr bool kScaled = sizeof(PartT) == 2;
   constexpr int NW = THREADS / 64;
   __shared__ float red[NW];
   __shared__ __attribute__((aligned(16))) float acc_lds[THREADS * 4];
@@ -768,23 +803,26 @@ __global__ void __launch_bounds__(THREADS) merge_kernel(int n_parts, int rows, i
   if (m != -INFINITY) {
     int q = grp;
     for (; q + 3 * G < n_parts; q += 4 * G) {
-      float w[4];
+      float w[4], sc[4];
       f32x4 x[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        w[u] = lrow[(size_t)(q + u * G) * rows];
-        x[u] = *reinterpret_cast<const f32x4*>(o_parts + ((size_t)(q + u * G) * rows + row) * d + c);
+        const size_t pr = (size_t)(q + u * G) * rows + row;
+        w[u] = lse_parts[pr];
+        sc[u] = kScaled ? scale_parts[pr] : 1.f;
+        x[u] = load_part4(o_parts + pr * d + c);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const float e = __expf(w[u] - m);  // 0 for an empty part (lse = -inf)
-        acc += e * x[u];
+        acc += (kScaled ? e * sc[u] : e) * x[u];
         tot += e;
       }
     }
     for (; q < n_parts; q += G) {
-      const float e = __expf(lrow[(size_t)q * rows] - m);
-      acc += e * *reinterpret_cast<const f32x4*>(o_parts + ((size_t)q * rows + row) * d + c);
+      const size_t pr = (size_t)q * rows + row;
+      const float e = __expf(lse_parts[pr] - m);
+      acc += (kScaled ? e * scale_parts[pr] : e) * load_part4(o_parts + pr * d + c);
       tot += e;
     }
   }
@@ -810,19 +848,20 @@ __global__ void __launch_bounds__(THREADS) merge_kernel(int n_parts, int rows, i
   if (lse && tid == 0) lse[row] = tot > 0.f ? m + logf(tot) : -INFINITY;
 }
 
-template <typename OutT>
-hipError_t launch_merge_t(int n_parts, int rows, int d, const float* o_parts,
-                          const float* lse_parts, OutT* o, float* lse, hipStream_t stream) {
+template <typename OutT, typename PartT>
+hipError_t launch_merge_t(int n_parts, int rows, int d, const PartT* o_parts,
+                          const float* scale_parts, const float* lse_parts, OutT* o, float* lse,
+                          hipStream_t stream) {
   if (rows == 0) return hipSuccess;
   // few rows, many parts (the key splits of one generated token): spread
   // each row's parts over 1024 threads so every thread has few loads to wait
   // for; otherwise 256 threads per row
   if (rows < 256 && n_parts >= 16)
-    hipLaunchKernelGGL((merge_kernel<OutT, 1024>), dim3((unsigned)rows), dim3(1024), 0, stream,
-                       n_parts, rows, d, o_parts, lse_parts, o, lse);
+    hipLaunchKernelGGL((merge_kernel<OutT, 1024, PartT>), dim3((unsigned)rows), dim3(1024), 0,
+                       stream, n_parts, rows, d, o_parts, scale_parts, lse_parts, o, lse);
   else
-    hipLaunchKernelGGL((merge_kernel<OutT, 256>), dim3((unsigned)rows), dim3(256), 0, stream,
-                       n_parts, rows, d, o_parts, lse_parts, o, lse);
+    hipLaunchKernelGGL((merge_kernel<OutT, 256, PartT>), dim3((unsigned)rows), dim3(256), 0,
+                       stream, n_parts, rows, d, o_parts, scale_parts, lse_parts, o, lse);
   return hipGetLastError();
 }
 
@@ -848,7 +887,9 @@ DecodePlan plan_decode(const DecodeArgs& a, uint64_t max_workspace_bytes) {
   if (bps > 0) n_split = (nblk + bps - 1) / bps;
   // a workspace limit caps the splits (longer splits, the same kernels)
   const int64_t rows_total = (int64_t)a.n_q * a.n_new;
-  const uint64_t per_split = (uint64_t)rows_total * (a.head_dim + 1) * 4;
+  // per (split, row): fp32 O and LSE, or fp16 O, its scale and the LSE
+  const uint64_t per_row = pl.waves == 8 ? (uint64_t)a.head_dim * 2 + 8 : (uint64_t)(a.head_dim + 1) * 4;
+  const uint64_t per_split = (uint64_t)rows_total * per_row;
   if ((uint64_t)n_split * per_split > max_workspace_bytes) {
     const int64_t cap = (int64_t)(max_workspace_bytes / per_split);
     if (cap < 1) {
@@ -902,8 +943,20 @@ hipError_t launch_decode(const DecodeArgs& a, const DecodePlan& pl, hipStream_t 
   DecParams p;
   p.q = a.q; p.kc = a.kc; p.vc = a.vc; p.kn = a.kn; p.vn = a.vn;
   const int64_t rows_total = (int64_t)a.n_q * a.n_new;
-  p.part_o = a.workspace;
-  p.part_lse = a.workspace + (size_t)pl.n_split * rows_total * a.head_dim;
+  const size_t parts = (size_t)pl.n_split * rows_total;  // (split, row) pairs
+  if (pl.waves == 8) {
+    // fp16 O, then the scales, then the LSEs
+    p.part_o = nullptr;
+    p.part_h = reinterpret_cast<uint16_t*>(a.workspace);
+    p.part_scale = reinterpret_cast<float*>(p.part_h + parts * a.head_dim);
+    p.part_lse = p.part_scale + parts;
+  } else {
+    // fp32 O, then the LSEs
+    p.part_o = a.workspace;
+    p.part_h = nullptr;
+    p.part_scale = nullptr;
+    p.part_lse = a.workspace + parts * a.head_dim;
+  }
   p.Lc = a.Lc; p.n_new = a.n_new; p.append = a.append; p.n_kv = a.n_kv;
   p.R = (a.n_q / a.n_kv) * a.n_new;
   p.rows_total = (int)rows_total;
@@ -920,13 +973,17 @@ hipError_t launch_decode(const DecodeArgs& a, const DecodePlan& pl, hipStream_t 
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_merge_t<float>(pl.n_split, (int)rows_total, a.head_dim, p.part_o, p.part_lse,
-                               a.o, a.lse, stream);
+  if (pl.waves == 8)
+    return launch_merge_t(pl.n_split, (int)rows_total, a.head_dim,
+                          reinterpret_cast<const _Float16*>(p.part_h), p.part_scale, p.part_lse,
+                          a.o, a.lse, stream);
+  return launch_merge_t(pl.n_split, (int)rows_total, a.head_dim, p.part_o,
+                        static_cast<const float*>(nullptr), p.part_lse, a.o, a.lse, stream);
 }
 
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream) {
-  return launch_merge_t<uint16_t>(a.n_parts, a.rows, a.head_dim, a.o_parts, a.lse_parts, a.o,
-                                  a.lse, stream);
+  return launch_merge_t<uint16_t, float>(a.n_parts, a.rows, a.head_dim, a.o_parts, nullptr,
+                                         a.lse_parts, a.o, a.lse, stream);
 }
 
 }  // namespace apb

@@ -51,8 +51,9 @@ struct DecodeArgs {
   float scale_log2;
 };
 
-// How a decode call splits its keys; the workspace holds one fp32 partial
-// (O and LSE) per split and row.
+// How a decode call splits its keys; the workspace holds one partial per
+// split and row: fp32 O and LSE (one-wave workgroups), or fp16 O with a
+// per-row power-of-two scale and the LSE (eight-wave workgroups).
 struct DecodePlan {
   int n_split;
   int blocks_per_split;
@@ -117,7 +118,7 @@ DecodePlan plan_decode(const DecodeArgs& a, uint64_t max_workspace_bytes = ~0ull
 hipError_t launch_decode(const DecodeArgs& a, const DecodePlan& pl, hipStream_t stream);
 // The no-allocation decode call's device scratch on the current device (its
 // address, looked up once per device), kDecodeScratchBytes long.
-constexpr uint64_t kDecodeScratchBytes = uint64_t(32) << 20;
+constexpr uint64_t kDecodeScratchBytes = uint64_t(16) << 20;
 hipError_t decode_scratch(void** ptr);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
 uint64_t scorer_workspace_bytes(const ScorerArgs& a);

@@ -166,8 +166,8 @@ def test_validate_decode(kw, code):
 
 
 def test_decode_workspace_size_is_shape_only():
-    # one fp32 partial (O and LSE) per split and row; more keys never need
-    # less scratch per row, and the size is a multiple of 16 bytes
+    # one fp32 partial (O and LSE) per split and row on the one-wave path (few
+    # rows per KV head); more keys never need less scratch per row
     rows = 8 * 3
     sizes = []
     for lc in (0, 1, 31, 32, 1000, 16384, 65536):
@@ -175,6 +175,11 @@ def test_decode_workspace_size_is_shape_only():
         assert n > 0 and n % (rows * 129 * 4) == 0
         sizes.append(n // (rows * 129 * 4))
     assert sizes == sorted(sizes) and sizes[0] == 1
+    # 256 rows per KV head: the eight-wave path, fp16 O + scale + LSE per row
+    rows = 32 * 64
+    for lc in (0, 100, 16384):
+        n = apb.decode_workspace_size(_dprob(n_q_heads=32, n_kv_heads=8, n_new=64, cache_len=lc))
+        assert n > 0 and n % (rows * (2 * 128 + 8)) == 0
     with pytest.raises(apb.ApbError):
         apb.decode_workspace_size(_dprob(head_dim=80))
     assert apb.lib().apb_decode_workspace_size(ctypes.byref(_dprob()), None) == 1
@@ -232,8 +237,10 @@ def test_decode_noalloc_error_paths():
     assert _dec_na(p, lse=DO + 16) == 6
     assert _dec_na(_dprob(head_dim=80)) == 3
     assert _dec_na(_dprob(n_new=0)) == 2
-    # one split's partials (rows * (d + 1) * 4 bytes) beyond the scratch
-    rows_max = apb.NOALLOC_SCRATCH_BYTES // (129 * 4)
+    # one split's partials beyond the scratch: 256 or more rows per KV head
+    # take the eight-wave path, whose partial per row is fp16 O (2d bytes),
+    # its scale and the LSE
+    rows_max = apb.NOALLOC_SCRATCH_BYTES // (2 * 128 + 8)
     big = _dprob(n_q_heads=8, n_kv_heads=8, n_new=rows_max // 8 + 1)
     assert _dec_na(big) == 7
     assert apb.lib().apb_status_string(7).startswith(b"the call needs more device scratch")

@@ -19,9 +19,9 @@ from gpu_util import assert_attention_close, dev_bf16, need_gpu, say
 pytestmark = pytest.mark.gpu
 
 # n_q, n_kv, d, Lc, n_new, append, capped: the first problem's default plan
-# needs 8 splits of 8192 rows (33.8 MB > the 32 MiB scratch) and runs with 7;
-# the second is the 128K Llama-8B-shaped question step (27.5 MB, fits); the
-# third a small one-wave problem.
+# needs 8 splits of 8192 rows (eight-wave path, fp16 partials: 17.3 MB > the
+# 16 MiB scratch) and runs with 7; the second is the 128K Llama-8B-shaped
+# question step (14.1 MB, fits); the third a small one-wave problem.
 CALLS = [
     (64, 8, 128, 16384, 128, 1, True),
     (32, 8, 128, 16384, 64, 1, False),
