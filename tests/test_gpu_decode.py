@@ -74,6 +74,38 @@ def test_decode_matches_oracle(shape):
     assert_attention_close(o, lse, o_ref, lse_ref, f"decode {shape}")
 
 
+def _scale_bf16(bits, k):
+    """bf16 bits of the values times 2**k (exact while nothing overflows)."""
+    x = inputs.bf16_bits_to_f32(bits).astype(np.float64) * 2.0 ** k
+    out = inputs.f32_to_bf16_bits(x.astype(np.float32))
+    assert np.array_equal(inputs.bf16_bits_to_f32(out).astype(np.float64), x)
+    return out
+
+
+@pytest.mark.parametrize("shape", [(8, 2, 128, 1000, 64, 1), (4, 1, 64, 300, 200, 0)])
+def test_decode_split_partials_follow_the_scale_of_v(shape):
+    """The eight-wave path (256 rows per KV head) keeps its split partials in
+    fp16 against a per-row power-of-two scale: every step is then exact under
+    V -> 2^k V, so O scales bit for bit and the LSE does not move, for values
+    far outside fp16's range (2^16 times N(0,1)) and deep in its subnormals
+    (2^-24 times)."""
+    n_q, n_kv, d, lc, n_new, app = shape
+    assert (n_q // n_kv) * n_new >= 128
+    say(f"[decode V scale] {shape}")
+    case = inputs.make_decode_case(n_q, n_kv, d, [lc], n_new, seed=23)
+    kc, vc = case["caches"][0]
+    kn = case["k_new"] if app else None
+    vn = case["v_new"] if app else None
+    o, lse = _run_decode(case["q"], kc, vc, kn, vn, n_q, n_kv, d)
+    o_ref, lse_ref = oracle.decode_attention_ref(case["q"], kc, vc, kn, vn)
+    assert_attention_close(o, lse, o_ref, lse_ref, f"decode V scale {shape}")
+    for k in (16, -24):
+        o_k, lse_k = _run_decode(case["q"], kc, _scale_bf16(vc, k), kn,
+                                 _scale_bf16(vn, k) if app else None, n_q, n_kv, d)
+        assert np.array_equal(o_k, o * 2.0 ** k), k
+        assert np.array_equal(lse_k, lse), k
+
+
 def test_decode_no_keys_rows():
     # no cache and nothing appended: every row sees nothing -> o = 0, lse = -inf
     case = inputs.make_decode_case(4, 2, 128, [0], 2, seed=3)
