@@ -192,7 +192,6 @@ attn_fwd_kernel(Params p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave / kGroupWaves;  // 0: group A, 1: group B
   const int wig = wave % kGroupWaves;  // wave in group
-  const int n = lane & 31, h = lane >> 5;
 
   int head, qtile;
   map_block(p, blockIdx.x, head, qtile);
