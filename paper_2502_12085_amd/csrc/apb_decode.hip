@@ -762,13 +762,13 @@ __global__ void __launch_bounds__(512) decode_pingpong_kernel(DecParams p) {
 __device__ __forceinline__ f32x4 load_part4(const float* q) {
   return *reinterpret_cast<const f32x4*>(q);
 }
-__device__ __forceinline__ f32x4 load_part4(const _Float16* q) {
+__device__ __forceinline__ f32x4 load_part4(const uint16_t* q) {  // fp16 bits
   const f16x4 v = *reinterpret_cast<const f16x4*>(q);
   return f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
 }
 
-// PartT: float parts, or _Float16 parts whose row r of part q is O divided
-// by scale_parts[q * rows + r].
+// PartT: float parts, or uint16_t parts holding the bits of fp16 values,
+// whose row r of part q is O divided by scale_parts[q * rows + r].
 template <typename OutT, int THREADS, typename PartT>
 __global__ void __launch_bounds__(THREADS) merge_kernel(int n_parts, int rows, int d,
                                                         const PartT* __restrict__ o_parts,
@@ -975,7 +975,7 @@ hipError_t launch_decode(const DecodeArgs& a, const DecodePlan& pl, hipStream_t 
   if (e != hipSuccess) return e;
   if (pl.waves == 8)
     return launch_merge_t(pl.n_split, (int)rows_total, a.head_dim,
-                          reinterpret_cast<const _Float16*>(p.part_h), p.part_scale, p.part_lse,
+                          static_cast<const uint16_t*>(p.part_h), p.part_scale, p.part_lse,
                           a.o, a.lse, stream);
   return launch_merge_t(pl.n_split, (int)rows_total, a.head_dim, p.part_o,
                         static_cast<const float*>(nullptr), p.part_lse, a.o, a.lse, stream);
