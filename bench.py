@@ -346,6 +346,10 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float =
     keys = lc + n_new
     dec_bytes = 2 * rows * d + 2 * 2 * n_kv * keys * d + 4 * rows * d + 4 * rows
     mrg_bytes = H * rows * (d + 1) * 4 + rows * d * 2 + rows * 4
+    # 4d flops per visible (row, key) pair: on the last host new token j sees
+    # the cache and new tokens 0..j
+    pairs = n_new * lc + n_new * (n_new + 1) // 2
+    dec_flops = 4.0 * d * n_q * pairs
     cpu = None
     if cpu_budget > 0:
         import oracle
@@ -365,6 +369,9 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float =
             "decode_us": round(dec_us, 2), "decode_algorithmic_bytes": dec_bytes,
             "decode_gbs": round(dec_bytes / (dec_us * 1e-6) / 1e9, 1),
             "decode_hbm_frac": round(dec_bytes / (dec_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "decode_flops": dec_flops,
+            "decode_mfma_frac": round(dec_flops / (dec_us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "arithmetic_intensity": round(dec_flops / dec_bytes, 1),
             "merge_us": round(mrg_us, 2), "merge_algorithmic_bytes": mrg_bytes,
             # the library's plan: eight-wave ping-pong workgroups once a GQA
             # group has four 32-row blocks, one-wave workgroups below that
