@@ -426,3 +426,51 @@ def test_simulated_hosts_end_to_end():
         np.testing.assert_array_equal(host_bits(kbuf[:p.host_idx]), rkp)
         np.testing.assert_array_equal(host_bits(vbuf[p.host_idx]), rvc)
         assert_attention_close(host_bf16_to_f64(o)[heads], lse.cpu().numpy()[heads], ro, rl, name)
+
+
+def test_compressor_and_attention_concurrent_on_two_streams():
+    """One host's compressor writes slot host_idx of the rank-major passing
+    buffer while its attention reads slots [0, host_idx) of the same buffer
+    (bench.py --overlap): run on two streams at once, in both launch orders,
+    every output matches the serial run bit for bit (both kernels are
+    deterministic, and neither touches what the other writes)."""
+    torch = need_gpu()
+    from paper_2502_12085_amd import apb
+    wl = _wl("llama8b_32k", n_q_heads=16, n_kv_heads=4)
+    p = wl.problem
+    say(f"[two streams] {p}")
+    inp = inputs.make_inputs(wl, 5)
+    dv = upload(inp)
+    H, n_kv, lp, d = p.n_hosts, p.n_kv_heads, p.pass_len, p.head_dim
+    kbuf = torch.zeros((H, n_kv, lp, d), dtype=torch.bfloat16, device="cuda")
+    vbuf = torch.zeros_like(kbuf)
+    kbuf[:p.host_idx] = dv["k_pass"]
+    vbuf[:p.host_idx] = dv["v_pass"]
+
+    def run(order, s_att, s_cmp):
+        kbuf[p.host_idx].zero_()
+        vbuf[p.host_idx].zero_()
+        idx = torch.full((n_kv, lp), -1, dtype=torch.int32, device="cuda")
+        o = torch.full((p.n_q_heads, p.rows, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((p.n_q_heads, p.rows), float("nan"), dtype=torch.float32, device="cuda")
+        torch.cuda.synchronize()
+        calls = {
+            "att": lambda: apb.attention_fwd(p, dv["q"], dv["k"], dv["v"], kbuf, vbuf, o, lse,
+                                             0.0, s_att),
+            "cmp": lambda: apb.compress_select(p, dv["scores"], dv["k"], dv["v"], idx,
+                                               kbuf[p.host_idx], vbuf[p.host_idx], s_cmp),
+        }
+        for name in order:
+            calls[name]()
+        torch.cuda.synchronize()
+        return (host_bits(o), lse.cpu().numpy(), idx.cpu().numpy(), host_bits(kbuf[p.host_idx]),
+                host_bits(vbuf[p.host_idx]))
+
+    main = torch.cuda.current_stream()
+    ref = run(("cmp", "att"), main, main)  # serial, one stream
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()  # default priority
+    for order in (("att", "cmp"), ("cmp", "att")):
+        got = run(order, s1, s2)
+        for a, b in zip(got, ref):
+            assert np.array_equal(a, b), order
+    assert np.all(ref[2] >= 0)
