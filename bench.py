@@ -115,6 +115,25 @@ def busy_ahead(stream, ms: float = 20.0) -> None:
     torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
 
 
+def warm_up(step, min_steps: int, seconds: float = 0.2) -> float:
+    """Run `step` (one synchronised call each) until at least `min_steps`
+    calls and `seconds` of them have passed, and return the last call's
+    milliseconds: from idle the shader clock takes some tens of milliseconds
+    of load to settle (measured: 30 ms of back-to-back 32K attention launches
+    ran up to 20% slower than the ones after), so a few short warm-up steps
+    would leave the timed ones on the way up."""
+    import torch
+    t0 = time.perf_counter()
+    n, last = 0, 0.0
+    while n < min_steps or time.perf_counter() - t0 < seconds:
+        t1 = time.perf_counter()
+        step()
+        torch.cuda.synchronize()
+        last = (time.perf_counter() - t1) * 1e3
+        n += 1
+    return last
+
+
 def parse_smi_metric(text: str):
     """Socket watts and the per-XCD shader clocks (MHz) from the text of
     `amd-smi metric -p -c` for one GPU: (None, []) where it prints neither."""
@@ -268,9 +287,7 @@ def bench_layer(lw, steps: int, warmup: int, seed: int = 0) -> dict:
     def call():
         apb.layer_fwd(lw, w, hidden, pos, kc, vc, pk, pv, out, ws, stream)
 
-    for _ in range(warmup):
-        call()
-    torch.cuda.synchronize()
+    warm_up(call, warmup)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     for e0, e1 in ev:
@@ -520,10 +537,9 @@ def bench_workload_row(name: str, steps: int, warmup: int, seed: int = 0,
         if e:
             e[2].record(stream)
 
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
-    busy_ahead(stream)
+    step_ms_warm = warm_up(step, warmup)
+    if step_ms_warm < 1.0:
+        busy_ahead(stream)  # few-microsecond steps: keep host gaps out of the events
     for e in ev:
         step(e)
     torch.cuda.synchronize()
@@ -571,7 +587,7 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama8b_128k")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=20.0,
