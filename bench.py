@@ -349,9 +349,7 @@ def bench_stage2(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float =
             events[2].record(stream)
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_up(step, warmup)
     busy_ahead(stream)
     for e in ev:
         step(e)
@@ -423,12 +421,11 @@ def bench_scorer(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float =
     ws = torch.empty(apb.scorer_workspace_size(sp), dtype=torch.uint8, device="cuda")
     scores = torch.empty((p.n_kv_heads, p.local_len), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
-    for _ in range(warmup):
-        apb.retaining_scores(sp, q, k, v, w1, b1, w2, b2, scores, ws, stream)
-    torch.cuda.synchronize()
+    warm_up(lambda: apb.retaining_scores(sp, q, k, v, w1, b1, w2, b2, scores, ws, stream), warmup)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
-    busy_ahead(stream)
+    # no spin ahead: a call is long beside its submission, and a spin would
+    # let the clock rise above what back-to-back calls hold
     for e0, e1 in ev:
         e0.record(stream)
         apb.retaining_scores(sp, q, k, v, w1, b1, w2, b2, scores, ws, stream)
@@ -461,7 +458,8 @@ def bench_scorer(wl, steps: int, warmup: int, seed: int = 0, cpu_budget: float =
             "tflops": round(tf, 1), "bound": "mfma", "peak": PEAK_BF16_TFLOPS,
             "frac": round(tf / PEAK_BF16_TFLOPS, 4),
             "kernel": "gemm_kernel<kXQkv, kWPlain, kEpiScorer> + scorer_reduce_kernel",
-            "timing": f"median of {steps} back-to-back launches, HIP events", "weights": "synthetic",
+            "timing": f"median of {steps} back-to-back launches after at least 0.2 s of warm-up "
+                      "launches, HIP events", "weights": "synthetic",
             "cpu_baseline": cpu}
 
 
