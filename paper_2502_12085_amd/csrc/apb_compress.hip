@@ -5,7 +5,8 @@
 // Design.  A grid of (S, n_kv) workgroups; workgroup (c, h) owns the local
 // index range chunk c of KV head h.  Every workgroup of a head first finds
 // the same selection threshold by an MSB-first radix select over all Lb
-// scores (four 8-bit digits of an order-preserving 32-bit key; the scores of
+// scores (digits of an order-preserving 32-bit key: four of 8 bits here, three
+// of 11, 11 and 10 bits in the register-resident kernel below; the scores of
 // one head are a few hundred KB at most and stay in L2), so no scratch memory,
 // atomics across workgroups or second launch are needed.  It then counts
 // what was selected before its chunk and compacts its chunk in index order
@@ -174,14 +175,15 @@ topk_gather_kernel(const float* __restrict__ scores, const uint16_t* __restrict_
 // LDS, 128 KiB, index-major so that a wave's reads are conflict-free; longer
 // local blocks use the kernel above).  1024 threads; thread t holds the keys
 // of local indices KPT*t .. KPT*t + KPT-1, loaded once with 16-byte vector
-// loads.  The radix select counts into one 256-bin
-// histogram per wave (LDS atomics collide only within a wave) and sums the
-// sixteen of them; the selected counts before each thread's range come from a
-// block scan.  Workgroup c of a head then gathers the selected rows whose
+// loads.  The radix select takes three digits of 11, 11 and 10 bits, each
+// counted into one shared 2048-bin histogram (wider digits spread the keys
+// of one wave's atomics over more addresses and save a pass); the selected
+// counts before each thread's range come from a block scan.  Workgroup c of a head then gathers the selected rows whose
 // output positions fall in its share [c*lp/S, (c+1)*lp/S).  Same threshold,
 // same tie rule, same output as the kernel above.
 constexpr int kRegThreads = 1024;
 constexpr int kRegWaves = kRegThreads / 64;
+constexpr int kSelBins = 2 * kRegThreads;  // 11-bit digits, two bins per thread
 
 template <int KPT>
 __global__ void __launch_bounds__(kRegThreads)
@@ -191,7 +193,8 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
                        int Lb, int lp, int head_dim, int share) {
   constexpr int KREG = KPT < 32 ? KPT : 32;  // keys per thread in registers
   constexpr int KLDS = KPT - KREG;           // keys per thread in LDS
-  __shared__ uint32_t hist[kRegWaves][256];
+  __shared__ uint32_t hist[kSelBins];
+  __shared__ uint32_t wtot[kRegWaves];
   __shared__ uint32_t wsum_gt[kRegWaves], wsum_eq[kRegWaves];
   __shared__ uint32_t sel_digit, sel_above;
   __shared__ int32_t list_src[1024];
@@ -230,50 +233,47 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
   list_src[tid] = -1;
 
   // ---- 1. radix select: key T of the lp-th largest score and `need`
+  // three digits of 11, 11 and 10 bits into one shared 2048-bin histogram;
+  // thread t owns bins 2t and 2t+1, reads and clears them after the counts
+  for (int b = tid; b < kSelBins; b += kRegThreads) hist[b] = 0u;
+  __syncthreads();
   uint32_t prefix = 0u, prefix_mask = 0u, remaining = (uint32_t)lp;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int b = lane; b < 256; b += 64) hist[wave][b] = 0u;
-    __syncthreads();
+#pragma unroll
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+    const uint32_t dmask = pass == 2 ? 1023u : 2047u;
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
       const uint32_t kj = get(j);
-      if (j < n_valid && (kj & prefix_mask) == prefix)
-        atomicAdd(&hist[wave][(kj >> shift) & 255u], 1u);
+      if (j < n_valid && (kj & prefix_mask) == prefix) atomicAdd(&hist[(kj >> shift) & dmask], 1u);
     }
     __syncthreads();
-    if (tid < 64) {
-      // lane L owns bins 4L..4L+3 (summed over the waves' histograms)
-      uint32_t c[4], own = 0u;
-      for (int j = 0; j < 4; ++j) {
-        uint32_t t = 0u;
-        for (int w = 0; w < kRegWaves; ++w) t += hist[w][4 * lane + j];
-        c[j] = t;
-        own += t;
-      }
-      uint32_t incl = own;  // inclusive suffix sum over lanes >= lane
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t o = __shfl_down(incl, off);
-        if (lane + off < 64) incl += o;
-      }
-      const uint32_t above_lane = incl - own;
-      if (above_lane < remaining && remaining <= incl) {
-        uint32_t above = above_lane;
-        for (int j = 3; j >= 0; --j) {
-          if (remaining <= above + c[j]) {
-            sel_digit = (uint32_t)(4 * lane + j);
-            sel_above = above;
-            break;
-          }
-          above += c[j];
-        }
+    const uint32_t c0 = hist[2 * tid], c1 = hist[2 * tid + 1];
+    hist[2 * tid] = 0u;
+    hist[2 * tid + 1] = 0u;
+    const uint32_t own = c0 + c1;
+    uint32_t incl = own;  // inclusive suffix sum over the lanes >= lane
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t o = __shfl_down(incl, off);
+      if (lane + off < 64) incl += o;
+    }
+    if (lane == 0) wtot[wave] = incl;
+    __syncthreads();
+    for (int w = wave + 1; w < kRegWaves; ++w) incl += wtot[w];
+    const uint32_t above_t = incl - own;  // keys in the bins above 2t+1
+    if (above_t < remaining && remaining <= incl) {
+      if (remaining <= above_t + c1) {
+        sel_digit = (uint32_t)(2 * tid + 1);
+        sel_above = above_t;
+      } else {
+        sel_digit = (uint32_t)(2 * tid);
+        sel_above = above_t + c1;
       }
     }
     __syncthreads();
     prefix |= sel_digit << shift;
-    prefix_mask |= 255u << shift;
+    prefix_mask |= dmask << shift;
     remaining -= sel_above;
-    __syncthreads();
   }
   const uint32_t T = prefix;
   const uint32_t need = remaining;
