@@ -185,6 +185,20 @@ constexpr int kRegThreads = 1024;
 constexpr int kRegWaves = kRegThreads / 64;
 constexpr int kSelBins = 2 * kRegThreads;  // 11-bit digits, two bins per thread
 
+// Inclusive prefix sum over the 64 lanes of a wave: shifts inside each
+// 16-lane row through DPP, then the three row totals taken by readlane.
+__device__ __forceinline__ uint32_t wave_prefix_sum(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
+}
+
 template <int KPT>
 __global__ void __launch_bounds__(kRegThreads)
 topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restrict__ k,
@@ -252,14 +266,13 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
     hist[2 * tid] = 0u;
     hist[2 * tid + 1] = 0u;
     const uint32_t own = c0 + c1;
-    uint32_t incl = own;  // inclusive suffix sum over the lanes >= lane
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t o = __shfl_down(incl, off);
-      if (lane + off < 64) incl += o;
-    }
-    if (lane == 0) wtot[wave] = incl;
+    const uint32_t pre = wave_prefix_sum(own);  // bins of the lanes <= lane
+    const uint32_t wt = (uint32_t)__builtin_amdgcn_readlane((int)pre, 63);
+    uint32_t incl = wt - pre + own;  // inclusive suffix sum over the lanes >= lane
+    if (lane == 0) wtot[wave] = wt;
     __syncthreads();
-    for (int w = wave + 1; w < kRegWaves; ++w) incl += wtot[w];
+#pragma unroll
+    for (int w = 1; w < kRegWaves; ++w) incl += w > wave ? wtot[w] : 0u;
     const uint32_t above_t = incl - own;  // keys in the bins above 2t+1
     if (above_t < remaining && remaining <= incl) {
       if (remaining <= above_t + c1) {
@@ -286,15 +299,15 @@ topk_gather_reg_kernel(const float* __restrict__ scores, const uint16_t* __restr
     n_gt += (j < n_valid && kj > T) ? 1u : 0u;
     n_eq += (j < n_valid && kj == T) ? 1u : 0u;
   }
-  uint32_t x_gt = n_gt, x_eq = n_eq;  // inclusive wave scans
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t a = __shfl_up(x_gt, off), b = __shfl_up(x_eq, off);
-    if (lane >= off) { x_gt += a; x_eq += b; }
-  }
+  const uint32_t x_gt = wave_prefix_sum(n_gt), x_eq = wave_prefix_sum(n_eq);  // inclusive
   if (lane == 63) { wsum_gt[wave] = x_gt; wsum_eq[wave] = x_eq; }
   __syncthreads();
   uint32_t gt_before = x_gt - n_gt, eq_before = x_eq - n_eq;
-  for (int w = 0; w < wave; ++w) { gt_before += wsum_gt[w]; eq_before += wsum_eq[w]; }
+#pragma unroll
+  for (int w = 0; w < kRegWaves - 1; ++w) {
+    gt_before += w < wave ? wsum_gt[w] : 0u;
+    eq_before += w < wave ? wsum_eq[w] : 0u;
+  }
 
   // ---- 3. this workgroup's share of output positions: its list in LDS
   const int p0 = blockIdx.x * share, p1 = min(lp, p0 + share);
