@@ -36,9 +36,10 @@
 //    start of its softmax phases, group A copies V early in its MFMA phases
 //    (behind the phase's first operand reads), each with two phases to land.
 //  * LDS tiles are row-major with an XOR swizzle of their 16-byte chunks: the
-//    K operand reads (ds_read_b128) and the transposing V operand reads
-//    (ds_read_b64_tr_b16) are free of bank conflicts, and each read address
-//    is one XOR of a per-lane base plus an immediate.
+//    K operand reads (ds_read_b128) are free of bank conflicts, the
+//    transposing V operand reads (ds_read_b64_tr_b16) two-way conflicted on
+//    purpose (see the layout note below), and each read address is one XOR
+//    of a per-lane base plus an immediate.
 //  * Online softmax in fp32 registers in base 2 (scale*log2(e) folded into one
 //    FMA), probabilities rounded to bf16 for the PV product, fp32 accumulate,
 //    taken one 32-key block at a time (few live temporaries).  The running
@@ -130,12 +131,17 @@ __device__ __forceinline__ const uint16_t* key_row_sel(const Params& p, const ui
 }
 
 // LDS tile layouts: row-major [kBN][D] bf16, 16-byte chunk c of row r stored
-// at chunk position c ^ swz(r).
-//  K: swz = r mod (D/8): the 16 rows one ds_read_b128 pass touches hit 16
-//     different chunk positions.
-//  V: swz = 4 * (r mod 4) (D = 128): the 16 lanes of a transposing read
-//     touch 4 rows x 32 bytes (two chunks each), which land on 8 different
-//     chunk positions.
+// at chunk position c ^ swz(r).  The LDS has 64 four-byte banks; a
+// ds_read_b128 serves 16 lanes per clock, a ds_read_b64_tr_b16 32 lanes.
+//  K: swz = r mod (D/8): the 16 rows one ds_read_b128 clock touches hit 16
+//     different chunk positions (no bank conflicts).
+//  V: swz = 4 * (r mod 4) (D = 128): the 16 lanes of one row group of a
+//     transposing read touch 4 rows x 32 bytes on 4 different bank groups;
+//     the 32 lanes of one clock cover rows r and r + 4 on the same banks, a
+//     two-way conflict.  It is kept on purpose: a swizzle free of conflicts
+//     (2 * (r mod 8)) gave bit-identical results but a 1.5-1.8% longer
+//     launch, the softmax waves losing issue slots to an MFMA wave that no
+//     longer stalls on its V reads.
 template <int D>
 __device__ __forceinline__ int k_swz(int r) { return r & (D / 8 - 1); }
 template <int D>
