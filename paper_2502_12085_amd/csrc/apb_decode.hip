@@ -81,10 +81,9 @@ __device__ __forceinline__ float half_swap(float x) {
 
 // LDS tile swizzles: 16-byte chunk c of key row r sits at chunk c ^ swz(r).
 // K: the 32 rows one ds_read_b128 pass touches hit distinct chunk slots;
-// V: the transposing reads of 4 rows x 4 chunks hit 16 distinct slots (rows
-// r and r + 4, which one 32-lane clock of the read serves together, share
-// banks: a two-way conflict, the layout the prefill kernel keeps because its
-// conflict-free alternative measured slower there).
+// V: the transposing reads of 4 rows x 4 chunks hit 16 distinct slots: the
+// 32 lanes one clock of such a read serves cover 4 rows x 64 bytes on 4
+// different 64-byte bank groups, so these reads are free of bank conflicts.
 template <int D>
 __device__ __forceinline__ int k_swz(int r) { return r & (D / 8 - 1); }
 template <int D>
