@@ -5,10 +5,11 @@ and the CPU check that these inputs really take that path.
 With N(0, 1) inputs and the default scale 1/sqrt(d) a row's max is set on
 its first tile and never passes the 2^13 sum limit later, so the parity
 cases use ``softmax_scale = 1.0`` (logits sqrt(d) times wider) and, in one
-case, a key planted late in the sequence along a query: its logit is about
-460 base-2 units above the others of that row, so the probabilities taken
-against the stale max overflow to +inf and the sum check has to catch an
-infinite sum, not just a large one.
+case, a key planted late in the sequence along a query.  That key's logit
+sits about 40 base-2 units above the rest of its row at the default scale
+(a finite stale probability near 2^40) and about 460 at scale 1.0, where the
+probabilities taken against the stale max overflow to +inf and the sum
+check has to catch an infinite sum, not just a large one.
 """
 import dataclasses
 
