@@ -135,6 +135,19 @@ def test_compress_error_paths():
     assert _comp(_prob(pass_len=0)) == 0
 
 
+def test_binding_raises_without_the_library(monkeypatch, tmp_path):
+    # no fallback: with libapb.so absent every call raises instead of
+    # computing anything elsewhere
+    monkeypatch.setattr(apb, "LIB_PATH", str(tmp_path / "libapb.so"))
+    monkeypatch.setattr(apb, "_lib", None)
+    with pytest.raises(RuntimeError, match="is missing"):
+        apb.lib()
+    with pytest.raises(RuntimeError, match="is missing"):
+        apb.attention_flops(inputs.WORKLOADS["tiny"].problem)
+    with pytest.raises(RuntimeError, match="is missing"):
+        apb.validate_problem(inputs.WORKLOADS["tiny"].problem)
+
+
 def test_binding_rejects_host_tensors():
     import torch
     x = torch.zeros(4, dtype=torch.bfloat16)
